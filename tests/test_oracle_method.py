@@ -1,0 +1,365 @@
+"""Pins of the oracle's quantizer and attention against what the paper fixes.
+
+Each test names the passage it follows.  None of them re-types the oracle's
+formula: they use closed forms, invariants, textbook attention, brute force
+on tiny inputs, or values worked out by hand from the definitions.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_33135_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+LAM = math.log2(math.e) / math.sqrt(128)
+
+
+def bf16_bits(x):
+    return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(torch.bfloat16) \
+        .view(torch.int16).numpy().view(np.uint16)
+
+
+def bits_to_f64(b):
+    return (np.asarray(b, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Constants the paper prints
+# ---------------------------------------------------------------------------
+
+def test_paper_constants(orc):
+    g = json.load(open(os.path.join(GOLDEN, "paper_constants.json")))
+    assert max(orc.e2m1_value(c) for c in range(8)) == g["rho"]["value"]
+    assert orc.e4m3_value(0x7E) == g["p_scale"]["value"]
+    # 1/2.56 of the BF16 KV footprint: (1/2 + 1/16) + 1 bytes vs 2 + 2 (Sec. 6)
+    k_bytes = 64 + 8          # NVFP4 codes + E4M3 scales per 128-channel row
+    v_bytes = 128
+    assert (k_bytes + v_bytes) / (2 * 128 * 2) == pytest.approx(1 / g["kv_ratio"]["value"])
+    # Delta_S side-cache share for GQA 32:8 (about 4% of KV bytes, Sec. 7.2)
+    share = 2 * 32 / (8 * (k_bytes + v_bytes) + 2 * 32)
+    assert abs(share - g["ds_share"]["value"]) < 0.005
+
+
+# ---------------------------------------------------------------------------
+# NVFP4 block quantizer (Sec. 2.1 Eq. 1) and the tensor scale
+# ---------------------------------------------------------------------------
+
+def test_tensor_scale_closed_form(orc):
+    rng = np.random.default_rng(0)
+    for a in np.concatenate([rng.lognormal(0, 6, 2000), [2688.0, 1344.0, 1.0, 5e-20, 3e15]]):
+        a = float(np.float32(a))
+        t = orc.tensor_scale(a)
+        assert math.frexp(t)[0] == 0.5                    # power of two
+        k = math.frexp(t)[1] - 1
+        if -64 < k < 64:
+            assert 2688.0 * t >= a and 1344.0 * t < a     # smallest such power
+        else:                                             # clamped exponent range
+            assert (k == -64 and 2688.0 * t >= a) or (k == 64 and 1344.0 * t < a)
+    assert orc.tensor_scale(0.0) == 1.0
+
+
+def test_nvfp4_hand_worked_blocks(orc):
+    """Hand-worked groups from tests/golden/nvfp4_blocks.json (Eq. 1, rho = 6)."""
+    cases = json.load(open(os.path.join(GOLDEN, "nvfp4_blocks.json")))["cases"]
+    for case in cases:
+        x = np.zeros(128, np.float32)
+        x[:16] = case["x"]
+        codes, scales = orc.nvfp4_row(x, case["t"])
+        assert scales[0] == int(case["scale_code"], 16), case["name"]
+        nib = [(codes[i // 2] >> (4 * (i % 2))) & 15 for i in range(16)]
+        assert nib == case["codes"], case["name"]
+
+
+def test_nvfp4_error_bound_and_idempotence(orc):
+    """|x - t s q| is at most half an E2M1 step of the group (or the clip of the
+    group maximum when its scale rounded down); dequantize -> requantize is a
+    fixed point."""
+    rng = np.random.default_rng(1)
+    for trial in range(300):
+        x = (rng.standard_normal(128) * rng.lognormal(0, 2)).astype(np.float32)
+        if trial % 3 == 0:
+            x[rng.integers(0, 128, 3)] *= 20
+        t = orc.tensor_scale(float(np.abs(x).max()))
+        codes, scales = orc.nvfp4_row(x, t)
+        deq = orc.nvfp4_dequant_row(codes, scales, t)
+        for g in range(8):
+            s = t * orc.e4m3_value(int(scales[g]))
+            xs = x[16 * g:16 * g + 16].astype(np.float64)
+            ds = deq[16 * g:16 * g + 16]
+            y = np.abs(xs) / s
+            step = np.where(y < 2, 0.5, np.where(y < 4, 1.0, 2.0)) * s
+            clipped = np.abs(xs) > 6 * s
+            ok = (np.abs(xs - ds) <= step / 2 + 1e-12 * np.abs(xs)) | (clipped & (np.abs(ds) == 6 * s))
+            assert ok.all(), (trial, g)
+            # the scale is the E4M3 value nearest to amax / (6 t)
+            ratio = np.float32(np.abs(x[16 * g:16 * g + 16]).max() / np.float32(6 * t))
+            cands = [orc.e4m3_value(c) for c in range(127)]
+            best = min(abs(c - ratio) for c in cands)
+            assert abs(orc.e4m3_value(int(scales[g])) - ratio) == best
+        codes2, scales2 = orc.nvfp4_row(deq.astype(np.float32), t)
+        nonzero = scales != 0
+        if nonzero.all():
+            assert np.array_equal(scales2, scales) and np.array_equal(codes2, codes)
+
+
+def test_nvfp4_zero_scale_keeps_signs(orc):
+    x = np.zeros(128, np.float32)
+    x[:16] = np.array([1e-30, -1e-30] * 8, np.float32)
+    codes, scales = orc.nvfp4_row(x, 1.0)
+    assert scales[0] == 0
+    assert codes[0] == 0x80       # element 0 (+) low nibble 0, element 1 (-) high nibble 8
+
+
+# ---------------------------------------------------------------------------
+# Statistics (Eq. 7) and Delta_S (Eq. 9)
+# ---------------------------------------------------------------------------
+
+def test_stats_constant_and_paired_columns(orc):
+    n = 300
+    x = np.zeros((n, 128), np.float32)
+    x[:, 0] = 1.5                                  # constant column -> exact
+    x[:, 1] = np.where(np.arange(n) % 2 == 0, 3.25, -3.25)   # +-pairs cancel exactly
+    x[:, 2] = np.linspace(-2, 2, n)
+    mean, t = orc.stats_one(bf16_bits(x), smooth=True)
+    m = bits_to_f64(mean)
+    assert m[0] == 1.5 and m[1] == 0.0 and m[3] == 0.0
+    xb = bits_to_f64(bf16_bits(x))
+    assert abs(m[2] - xb[:, 2].mean()) <= 2.0 ** -8 * max(abs(xb[:, 2].mean()), 1e-3)
+    amax = np.abs(xb - m[None, :]).max()
+    assert 2688 * t >= amax > 1344 * t
+
+
+def test_stats_match_fp64_mean(orc):
+    rng = np.random.default_rng(2)
+    x = (rng.standard_normal((1000, 128)) + rng.standard_normal(128) * 3).astype(np.float32)
+    xb = bf16_bits(x)
+    mean, _ = orc.stats_one(xb, smooth=True)
+    ref = bits_to_f64(xb).reshape(1000, 128).mean(0)
+    got = bits_to_f64(mean)
+    assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-6)
+
+
+def _quant_small(orc, seed, n, h_q=1, h_kv=1, flags=None, zero_mean=False, outliers=False):
+    q = W.gen_tensor(seed, W.STREAM_Q, 0, 0, n, h_q, outliers=outliers, out_stream=W.STREAM_OUT_Q)
+    off = W.k_offsets(seed, h_kv)
+    k = W.gen_tensor(seed, W.STREAM_K, 0, 0, n, h_kv, outliers=outliers, out_stream=W.STREAM_OUT_K,
+                     offset=off)
+    v = W.gen_tensor(seed, W.STREAM_V, 0, 0, n, h_kv)
+    if zero_mean:   # exact +-pairs: every channel sums to zero
+        q[1::2] = -q[0::2]
+        k[1::2] = -k[0::2]
+    qb = q.view(torch.int16).numpy().view(np.uint16)
+    kb = k.view(torch.int16).numpy().view(np.uint16)
+    vb = v.view(torch.int16).numpy().view(np.uint16)
+    n_pages = (n + 63) // 64
+    slots = np.arange(n, dtype=np.int64)
+    if flags is None:
+        flags = orc.SMOOTH | orc.COMPUTE_STATS
+    res = orc.quantize_qk(qb, kb, vb, [0, n], slots, n_pages, flags)
+    return qb, kb, vb, res
+
+
+def test_delta_s_matches_fp64_dot(orc):
+    qb, kb, vb, r = _quant_small(orc, 11, 200, h_q=4, h_kv=2)
+    qm = bits_to_f64(r["q_mean"][0])          # [4][128]
+    km = bits_to_f64(r["k_mean"][0])          # [2][128]
+    k = bits_to_f64(kb).reshape(200, 2, 128)
+    kc = (k.astype(np.float32) - km.astype(np.float32)[None]).astype(np.float64)
+    for h in range(4):
+        ref = kc[:, h // 2, :] @ qm[h]
+        ds = bits_to_f64(r["cache"]["ds"][:, h, :].reshape(-1)[:200])
+        err = np.abs(ds - ref)
+        assert np.all(err <= 2.0 ** -8 * np.abs(ref) + 1e-5 * (np.abs(kc[:, h // 2]) @ np.abs(qm[h])))
+
+
+def test_zero_mean_input_makes_compensation_vanish(orc):
+    """Zero-mean Q and K: Qbar = Kbar = 0, Delta_S == +0 everywhere, and the
+    smoothed path equals the direct path bit for bit (Sec. 4.3)."""
+    n = 256
+    qb, kb, vb, on = _quant_small(orc, 3, n, zero_mean=True)
+    _, _, _, off = _quant_small(orc, 3, n, flags=orc.COMPUTE_STATS, zero_mean=True)
+    assert not on["q_mean"].any() and not on["k_mean"].any()
+    assert not on["cache"]["ds"].any()            # +0 bit pattern everywhere
+    for key in ("k_codes", "k_scales", "v_codes"):
+        assert np.array_equal(on["cache"][key], off["cache"][key])
+    assert np.array_equal(on["q_codes"], off["q_codes"])
+    items = np.array([(0, i, 0) for i in range(0, n, 5)], np.int32)
+    pt = np.arange(4, dtype=np.int32)[None]
+    a, _ = orc.prefill(on["cache"], pt, [n], on["k_tscale"], on["q_codes"], on["q_scales"],
+                       on["q_tscale"], [0, n], [0], items, smooth=True)
+    b, _ = orc.prefill(off["cache"], pt, [n], off["k_tscale"], off["q_codes"], off["q_scales"],
+                       off["q_tscale"], [0, n], [0], items, smooth=False)
+    assert np.array_equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# Attention core with quantization off: exact softmax attention (Eq. 2)
+# ---------------------------------------------------------------------------
+
+def _rand_qkv(rng, nq, nk, scale=1.0):
+    q = rng.standard_normal((nq, 128)) * scale
+    k = rng.standard_normal((nk, 128)) * scale + rng.standard_normal(128) * 2
+    v = rng.standard_normal((nk, 128))
+    return q, k, v
+
+
+def test_online_softmax_equals_textbook(orc):
+    rng = np.random.default_rng(5)
+    q, k, v = _rand_qkv(rng, 40, 300)
+    pos = np.sort(rng.integers(0, 300, 40))
+    ref = orc.attention_textbook(q, k, v, pos)
+    for flags in (orc.REVERSE, 0):
+        for tile in (128, 64, 7):
+            got = orc.attention_f64(q, k, v, None, pos, tile=tile, flags=flags)
+            assert np.max(np.abs(got - ref)) < 1e-12 * np.max(np.abs(ref)) + 1e-13
+
+
+def test_partitioned_merge_equals_textbook(orc):
+    rng = np.random.default_rng(6)
+    q, k, v = _rand_qkv(rng, 8, 1000)
+    ref = orc.attention_textbook(q, k, v)
+    for part in (128, 256, 384, 1000, 4096):
+        got = orc.attention_f64(q, k, v, None, None, tile=128, partition=part, flags=orc.REVERSE)
+        assert np.max(np.abs(got - ref)) < 1e-12
+
+
+def test_smoothing_identity_eq8(orc):
+    """With quantization off, Q_c K_c^T + 1 (Qbar K_c^T) differs from Q K^T by a
+    row constant, so the smoothed attention equals exact attention for ANY
+    Qbar, Kbar (Eqs. 8-10)."""
+    rng = np.random.default_rng(7)
+    q, k, v = _rand_qkv(rng, 30, 400)
+    pos = np.sort(rng.integers(0, 400, 30))
+    ref = orc.attention_textbook(q, k, v, pos)
+    for _ in range(3):
+        qbar = rng.standard_normal(128) * 3
+        kbar = rng.standard_normal(128) * 3
+        qc, kc = q - qbar, k - kbar
+        ds = np.tile((kc @ qbar)[None, :], (30, 1))
+        got = orc.attention_f64(qc, kc, v, ds, pos, tile=128, flags=orc.REVERSE)
+        assert np.max(np.abs(got - ref)) < 1e-11
+        # without the compensation the result is wrong (the term is not row-constant)
+        bad = orc.attention_f64(qc, kc, v, None, pos, tile=128, flags=orc.REVERSE)
+        assert np.max(np.abs(bad - ref)) > 1e-3
+
+
+# ---------------------------------------------------------------------------
+# P quantization with the fixed scale 448 (Sec. 4.1)
+# ---------------------------------------------------------------------------
+
+def test_single_visible_key_returns_its_value(orc):
+    rng = np.random.default_rng(8)
+    q, k, v = _rand_qkv(rng, 1, 50)
+    vq = np.array([[orc.e4m3_value(int(c)) for c in row] for row in
+                   orc.e4m3_encode(v.astype(np.float32))])
+    got = orc.attention_f64(q, k, vq, None, np.array([0]), tile=128,
+                            flags=orc.REVERSE | orc.QUANT_P)
+    assert np.array_equal(got[0], vq[0])       # P = 1 -> code 448 -> exactly v
+
+
+def test_equal_scores_give_uniform_average(orc):
+    rng = np.random.default_rng(9)
+    v = rng.standard_normal((200, 128))
+    q = np.zeros((1, 128))
+    k = rng.standard_normal((200, 128))
+    got = orc.attention_f64(q, k, v, None, None, tile=128, flags=orc.REVERSE | orc.QUANT_P)
+    assert np.max(np.abs(got[0] - v.mean(0))) < 1e-13
+
+
+def test_p_quantization_error_bound(orc):
+    """Each P_hat/448 is within half an E4M3 step of P, so the output moves by at
+    most 2^-4 of the value range relative to the unquantized path."""
+    rng = np.random.default_rng(10)
+    q, k, v = _rand_qkv(rng, 20, 500, scale=0.5)
+    exact = orc.attention_f64(q, k, v, None, None, tile=128, flags=orc.REVERSE)
+    quant = orc.attention_f64(q, k, v, None, None, tile=128, flags=orc.REVERSE | orc.QUANT_P)
+    assert np.max(np.abs(quant - exact)) <= 2.0 ** -4 * np.max(np.abs(v)) * 2
+    assert np.max(np.abs(quant - exact)) > 0     # and it does quantize
+
+
+def test_reverse_traversal_changes_only_rounding(orc):
+    rng = np.random.default_rng(12)
+    q, k, v = _rand_qkv(rng, 10, 700)
+    fwd = orc.attention_f64(q, k, v, None, None, tile=128, flags=orc.QUANT_P)
+    rev = orc.attention_f64(q, k, v, None, None, tile=128, flags=orc.QUANT_P | orc.REVERSE)
+    exact = orc.attention_textbook(q, k, v)
+    assert np.max(np.abs(fwd - exact)) < 0.05 and np.max(np.abs(rev - exact)) < 0.05
+
+
+# ---------------------------------------------------------------------------
+# Paged cache bookkeeping, prefill vs decode, and the compensation benefit
+# ---------------------------------------------------------------------------
+
+def test_prefill_matches_dequantized_reference_and_page_shuffle(orc):
+    n = 320
+    qb, kb, vb, r = _quant_small(orc, 21, n, h_q=2, h_kv=1)
+    n_pages = 5
+    perm = np.array([3, 0, 4, 1, 2], np.int32)
+    slots = perm[np.arange(n) // 64].astype(np.int64) * 64 + np.arange(n) % 64
+    r2 = orc.quantize_qk(qb, kb, vb, [0, n], slots, n_pages, orc.SMOOTH | orc.COMPUTE_STATS)
+    items = np.array([(0, i, h) for i in range(0, n, 3) for h in range(2)], np.int32)
+    a, a64 = orc.prefill(r["cache"], np.arange(5, dtype=np.int32)[None], [n], r["k_tscale"],
+                         r["q_codes"], r["q_scales"], r["q_tscale"], [0, n], [0], items)
+    b, _ = orc.prefill(r2["cache"], perm[None], [n], r2["k_tscale"], r2["q_codes"],
+                       r2["q_scales"], r2["q_tscale"], [0, n], [0], items)
+    assert np.array_equal(a, b)
+    # the same numbers from dequantized arrays laid out directly in numpy
+    kc, ks, vc, ds = (r["cache"][x] for x in ("k_codes", "k_scales", "v_codes", "ds"))
+    kd = np.stack([orc.nvfp4_dequant_row(kc[j // 64, 0, j % 64], ks[j // 64, 0, j % 64],
+                                         r["k_tscale"][0, 0]) for j in range(n)])
+    vd = np.stack([[orc.e4m3_value(int(vc[j // 64, 0, c, j % 64])) for c in range(128)]
+                   for j in range(n)])
+    for h in range(2):
+        qd = np.stack([orc.nvfp4_dequant_row(r["q_codes"][i, h], r["q_scales"][i, h],
+                                             r["q_tscale"][0, h]) for i in range(n)])
+        dsd = bits_to_f64(ds[:, h, :].reshape(-1)[:n])
+        sel = items[:, 2] == h
+        rows = items[sel, 1]
+        ref = orc.attention_f64(qd[rows], kd, vd, np.tile(dsd, (len(rows), 1)), rows,
+                                tile=128, flags=orc.REVERSE | orc.QUANT_P)
+        assert np.max(np.abs(a64[sel] - ref)) < 1e-12
+
+
+def test_decode_equals_last_prefill_row(orc):
+    n = 384
+    qb, kb, vb, r = _quant_small(orc, 31, n, h_q=4, h_kv=2)
+    pt = np.arange(6, dtype=np.int32)[None]
+    items = np.array([(0, n - 1, h) for h in range(4)], np.int32)
+    pre, _ = orc.prefill(r["cache"], pt, [n], r["k_tscale"], r["q_codes"], r["q_scales"],
+                         r["q_tscale"], [0, n], [0], items)
+    qlast = r["q_codes"][n - 1:n]
+    dec, _ = orc.decode(r["cache"], pt, [n], r["k_tscale"], qlast, r["q_scales"][n - 1:n],
+                        r["q_tscale"], 512, np.array([(0, h) for h in range(4)], np.int32))
+    assert np.array_equal(pre, dec)
+    dec2, d64 = orc.decode(r["cache"], pt, [n], r["k_tscale"], qlast, r["q_scales"][n - 1:n],
+                           r["q_tscale"], 128, np.array([(0, h) for h in range(4)], np.int32))
+    assert np.max(np.abs(bits_to_f64(dec2) - bits_to_f64(pre))) < 0.05
+
+
+def test_compensation_lowers_error(orc):
+    """Over 12 seeds of the tiny workload recipe (per-channel K offsets), QK4PV8
+    with smoothing is closer to FP64 unquantized attention than QK4PV8 direct
+    (the accuracy claim of Sec. 4.2-4.3 / Table 2, as an operator-level
+    statistic)."""
+    n = 256
+    wins = 0
+    ratios = []
+    for seed in range(100, 112):
+        errs = []
+        for flags, smooth in ((orc.SMOOTH | orc.COMPUTE_STATS, True), (orc.COMPUTE_STATS, False)):
+            qb, kb, vb, r = _quant_small(orc, seed, n, flags=flags)
+            items = np.array([(0, i, 0) for i in range(n)], np.int32)
+            _, o64 = orc.prefill(r["cache"], np.arange(4, dtype=np.int32)[None], [n],
+                                 r["k_tscale"], r["q_codes"], r["q_scales"], r["q_tscale"],
+                                 [0, n], [0], items, smooth=smooth)
+            ref = orc.attention_textbook(bits_to_f64(qb).reshape(n, 128),
+                                         bits_to_f64(kb).reshape(n, 128),
+                                         bits_to_f64(vb).reshape(n, 128), np.arange(n))
+            errs.append(np.abs(o64 - ref).mean())
+        wins += errs[0] < errs[1]
+        ratios.append(errs[0] / errs[1])
+    assert wins >= 11 and np.mean(ratios) < 0.8, ratios
