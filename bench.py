@@ -1,0 +1,290 @@
+#!/usr/bin/env python3
+"""Benchmark of the QK4PV8 attention hot path on one MI355X.
+
+One step = the whole path over one batch of synthetic input:
+  * quantization / cache-write pass of the 128K-token Qwen3-14B-shaped causal
+    prefill (statistics, NVFP4 Q/K, FP8 V, Delta_S),
+  * the causal prefill over it (the headline: attention TFLOP/s),
+  * split-KV paged decode of the Llama-3.1-8B-shaped batch (32 sequences,
+    contexts U[16384, 131072]) over a pre-quantized, shuffled 64-token-page
+    cache (decode KV GB/s).
+Inputs are resident in HBM before the timed region; kernel times come from
+HIP events on the stream the kernels run on.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP4 = 10.0e15        # MI355X dense MXFP4 FLOP/s
+PEAK_FP8 = 5.0e15         # dense FP8
+PEAK_BF16 = 2.5e15        # dense BF16 / FP16
+PEAK_HBM = 8.0e12         # bytes/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--prefill-seq", type=int, default=131072)
+    ap.add_argument("--decode-batch", type=int, default=32)
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-direct", action="store_true", help="skip the unsmoothed prefill variant")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=4096, help="oracle sample: query rows of head 0")
+    return ap.parse_args()
+
+
+class Timer:
+    """HIP events on the current stream around a region."""
+
+    def __init__(self, torch):
+        self.t = torch
+        self.s = torch.cuda.Event(enable_timing=True)
+        self.e = torch.cuda.Event(enable_timing=True)
+
+    def __enter__(self):
+        self.s.record()
+        return self
+
+    def __exit__(self, *exc):
+        self.e.record()
+
+    def ms(self):
+        self.e.synchronize()
+        return self.s.elapsed_time(self.e)
+
+
+def setup_prefill(torch, np, mp, W, seq, smooth):
+    wl = W.qwen_prefill(seq)
+    dev = "cuda"
+    q, k, v = W.gen_qkv(wl.seed, [seq], wl.h_q, wl.h_kv, wl.outliers, dev)
+    pt, n_pages = W.make_pages(wl.seed, [seq])
+    slots = W.slots_for(pt, 0, range(seq))
+    d = lambda a: torch.from_numpy(a).to(dev)
+    st = dict(wl=wl, q=q, k=k, v=v, pt=pt, pt_d=d(pt), n_pages=n_pages,
+              cu=d(np.array([0, seq], np.int32)), slots=d(slots),
+              q_start=d(np.zeros(1, np.int32)), kv_len=d(np.array([seq], np.int32)),
+              cache=mp.PagedCache(n_pages, wl.h_q, wl.h_kv, dev, smooth=smooth),
+              stats=mp.SeqStats(1, wl.h_q, wl.h_kv, dev), qq=mp.QuantQ(seq, 1, wl.h_q, dev),
+              out=torch.empty((seq, wl.h_q, 128), dtype=torch.bfloat16, device=dev),
+              flags=(mp.SMOOTH if smooth else 0))
+    return st
+
+
+def run_quant(mp, st):
+    mp.quantize_qk(st["q"], st["k"], st["v"], st["cu"], st["slots"], st["cache"], st["stats"],
+                   st["qq"], st["flags"] | mp.COMPUTE_STATS, st["q"].shape[0])
+
+
+def run_prefill(mp, st):
+    mp.prefill(st["qq"], st["cache"], st["stats"], st["cu"], st["q_start"], st["kv_len"],
+               st["pt_d"], st["out"], st["q"].shape[0], st["flags"])
+
+
+def setup_decode(torch, np, mp, W, batch):
+    wl = W.llama_decode(batch)
+    dev = "cuda"
+    lens = wl.kv_len
+    pt, n_pages = W.make_pages(wl.seed, lens)
+    cache = mp.PagedCache(n_pages, wl.h_q, wl.h_kv, dev)
+    stats = mp.SeqStats(batch, wl.h_q, wl.h_kv, dev)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    # context cache write per sequence (statistics over the context, then frozen)
+    for b, n in enumerate(lens):
+        ctx = n - 1
+        q, k, v = W.gen_qkv(wl.seed, [ctx], wl.h_q, wl.h_kv, wl.outliers, dev, seq_ids=[b])
+        sb = mp.SeqStats(1, wl.h_q, wl.h_kv, dev)
+        qq = mp.QuantQ(ctx, 1, wl.h_q, dev)
+        slots = W.slots_for(pt, b, range(ctx))
+        mp.quantize_qk(q, k, v, d(np.array([0, ctx], np.int32)), d(slots), cache, sb, qq,
+                       mp.SMOOTH | mp.COMPUTE_STATS, ctx)
+        stats.q_mean[b].copy_(sb.q_mean[0])
+        stats.k_mean[b].copy_(sb.k_mean[0])
+        stats.k_tscale[b].copy_(sb.k_tscale[0])
+        del q, k, v, qq
+    torch.cuda.synchronize()
+    # the new token of every sequence: appended (frozen statistics), then queried
+    qn, kn, vn = W.gen_qkv(wl.seed, [1] * batch, wl.h_q, wl.h_kv, wl.outliers, dev,
+                           tok_offsets=[n - 1 for n in lens])
+    slots1 = np.array([W.slots_for(pt, b, [lens[b] - 1])[0] for b in range(batch)], np.int64)
+    qq = mp.QuantQ(batch, batch, wl.h_q, dev)
+    mp.quantize_qk(qn, kn, vn, d(np.arange(batch + 1, dtype=np.int32)), d(slots1), cache,
+                   stats, qq, mp.SMOOTH, 1)
+    part = mp.decode_choose_partition(lens, wl.h_kv, torch.cuda.get_device_properties(0).multi_processor_count)
+    maxp = max(math.ceil(n / part) for n in lens)
+    ws = torch.empty(mp.decode_workspace_size(batch, wl.h_q, maxp) // 4, dtype=torch.float32,
+                     device=dev)
+    out = torch.empty((batch, wl.h_q, 128), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    return dict(wl=wl, lens=lens, pt=pt, pt_d=d(pt), cache=cache, stats=stats, qq=qq, ws=ws,
+                out=out, kv_len=d(np.asarray(lens, np.int32)), part=part, maxp=maxp)
+
+
+def run_decode(mp, st):
+    mp.decode_paged(st["qq"], st["cache"], st["stats"], st["kv_len"], st["pt_d"], st["out"],
+                    st["part"], st["maxp"], st["ws"], mp.SMOOTH)
+
+
+def decode_bytes(st):
+    """Algorithmic bytes of one decode launch: K codes + scales + V codes + Delta_S of
+    every key, the quantized queries, the outputs, the page-table entries."""
+    wl = st["wl"]
+    keys = sum(st["lens"])
+    per_key = wl.h_kv * (64 + 8 + 128) + wl.h_q * 2
+    pages = sum(math.ceil(n / 64) for n in st["lens"])
+    return keys * per_key + wl.batch * wl.h_q * (72 + 4) + wl.batch * wl.h_q * 256 + pages * 4 \
+        + wl.batch * 4
+
+
+def cpu_baseline(np, W, st, rows):
+    """Time the CPU oracle (as it stands) on a bounded sample of the same prefill
+    workload: query head 0, `rows` query rows spread over the sequence."""
+    from oracle import oracle as orc
+    orc.build()
+    wl = st["wl"]
+    seq = st["q"].shape[0]
+    log(f"cpu baseline: oracle quantization of the {seq}-token workload ...")
+    ref = orc.quantize_qk(W.bits(st["q"]), W.bits(st["k"]), W.bits(st["v"]),
+                          np.array([0, seq], np.int32), W.slots_for(st["pt"], 0, range(seq)),
+                          st["n_pages"], orc.SMOOTH | orc.COMPUTE_STATS)
+    pos = np.unique(np.linspace(0, seq - 1, rows).astype(np.int64))
+    items = np.array([(0, int(i), 0) for i in pos], np.int32)
+    t0 = time.perf_counter()
+    orc.prefill(ref["cache"], st["pt"], [seq], ref["k_tscale"], ref["q_codes"], ref["q_scales"],
+                ref["q_tscale"], [0, seq], [0], items)
+    dt = time.perf_counter() - t0
+    flops = float(sum(4 * 128 * (int(i) + 1) for i in pos))
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": orc.num_threads(),
+            "kind": "oracle",
+            "sample": f"{len(pos)} query rows of head 0 (positions spread over 0..{seq - 1}), "
+                      f"{flops:.3e} FLOP in {dt:.2f} s; quantization not timed"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is "
+                                   "described in DESIGN.md but not built"}))
+        sys.exit(2)
+    import torch
+    import paper_2609_33135_amd as mp
+    from paper_2609_33135_amd import workloads as W
+    import numpy as np
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    mp.lib()
+    res = {}
+    prefill_ms = quant_ms = decode_ms = 0.0
+    seq = args.prefill_seq
+
+    if not args.no_prefill:
+        log(f"setup prefill {seq} tokens ...")
+        st = setup_prefill(torch, np, mp, W, seq, smooth=True)
+        for _ in range(args.warmup):
+            run_quant(mp, st)
+            run_prefill(mp, st)
+        torch.cuda.synchronize()
+        qt, pt_ = [], []
+        for _ in range(args.steps):
+            with Timer(torch) as t1:
+                run_quant(mp, st)
+            with Timer(torch) as t2:
+                run_prefill(mp, st)
+            qt.append(t1)
+            pt_.append(t2)
+        torch.cuda.synchronize()
+        quant_ms = sum(t.ms() for t in qt) / args.steps
+        prefill_ms = sum(t.ms() for t in pt_) / args.steps
+        wl = st["wl"]
+        pairs = wl.causal_pairs()
+        f_qk = 2.0 * 128 * pairs
+        f_pv = 2.0 * 128 * pairs
+        flops = f_qk + f_pv
+        achieved = flops / (prefill_ms * 1e-3)
+        roof_t = f_qk / PEAK_FP4 + f_pv / PEAK_FP8
+        peak = flops / roof_t
+        res["prefill"] = {"ms": prefill_ms, "tflops": achieved / 1e12, "quant_ms": quant_ms,
+                          "causal_pairs": pairs, "flop": flops}
+        res["roofline"] = {"bound": "mfma", "achieved": achieved / 1e12, "peak": peak / 1e12,
+                           "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                           "kernel": "prefill_kernel<true>",
+                           "peak_note": "time-weighted FP4 (QK) + FP8 (PV) dense peak; exact-NVFP4 "
+                                        "path peak (FP16 QK + FP8 PV) is "
+                                        f"{flops / (f_qk / PEAK_BF16 + f_pv / PEAK_FP8) / 1e12:.0f}"}
+        if not args.no_direct:
+            log("prefill direct (unsmoothed) variant ...")
+            del st["cache"]
+            std = setup_prefill(torch, np, mp, W, seq, smooth=False)
+            for _ in range(args.warmup):
+                run_quant(mp, std)
+                run_prefill(mp, std)
+            ts = []
+            for _ in range(args.steps):
+                run_quant(mp, std)
+                with Timer(torch) as t2:
+                    run_prefill(mp, std)
+                ts.append(t2)
+            torch.cuda.synchronize()
+            direct_ms = sum(t.ms() for t in ts) / args.steps
+            res["prefill"]["direct_ms"] = direct_ms
+            res["prefill"]["rank_one_overhead"] = prefill_ms / direct_ms - 1.0
+            del std
+        if not args.no_cpu_baseline:
+            res["cpu_baseline"] = cpu_baseline(np, W, st, args.cpu_rows)
+        del st
+        torch.cuda.empty_cache()
+
+    if not args.no_decode:
+        log(f"setup decode batch {args.decode_batch} ...")
+        sd = setup_decode(torch, np, mp, W, args.decode_batch)
+        for _ in range(args.warmup):
+            run_decode(mp, sd)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(args.steps):
+            with Timer(torch) as t:
+                run_decode(mp, sd)
+            ts.append(t)
+        torch.cuda.synchronize()
+        decode_ms = sum(t.ms() for t in ts) / args.steps
+        nbytes = decode_bytes(sd)
+        gbs = nbytes / (decode_ms * 1e-3) / 1e9
+        res["decode"] = {"ms": decode_ms, "GB/s": gbs, "frac_hbm": gbs * 1e9 / PEAK_HBM,
+                         "bytes": nbytes, "partition_tokens": sd["part"],
+                         "keys": int(sum(sd["lens"]))}
+
+    line = {
+        "metric": "prefill attn TFLOPS (causal 128K) + decode KV GB/s, % of roofline, 1 MI355X",
+        "value": res.get("prefill", {}).get("tflops"),
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": quant_ms + prefill_ms + decode_ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "nvfp4 via exact f16 mfma (QK) + fp8 mfma (PV), f32 softmax",
+        "data": "synthetic (seeded counter-based normal, per-channel K offsets, 0.1% x20 outliers)",
+        "config": {"workload": f"qwen3-14b-shaped causal prefill {seq} tokens 40q/8kv d128 + "
+                               f"llama-3.1-8b-shaped paged decode batch {args.decode_batch} "
+                               "contexts U[16384,131072] 32q/8kv d128",
+                   "prefill_seq": seq, "decode_batch": args.decode_batch, "page_tokens": 64,
+                   "smoothing": True},
+    }
+    line.update({k: v for k, v in res.items()})
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

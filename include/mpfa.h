@@ -1,0 +1,237 @@
+/*
+ * mpfa.h -- C ABI of the MI355X (gfx950) QK4PV8 FlashAttention library.
+ *
+ * The method (MpFA, "QK4PV8"): Q and K are centered per sequence and head and
+ * quantized to NVFP4 (E2M1 elements, one E4M3 scale per 16 head-dimension
+ * elements, Sec. 2.1 Eq. 1 and Sec. 4.1-4.2); the removed Q-mean term is
+ * restored as a rank-one contraction that seeds the score accumulator
+ * (Sec. 4.3 Eqs. 8-11); online softmax runs in FP32 (Sec. 2.2 Eqs. 3-6); P is
+ * quantized to FP8 E4M3 with the fixed scale 448 (Sec. 4.1); V is stored in
+ * FP8 E4M3 and PV runs on FP8 matrix cores; KV blocks are visited in reverse
+ * (Sec. 4.1).  Prefill is causal (Algorithm 1); decode is split-KV over a
+ * paged cache with a log-sum-exp merge (Sec. 5.3, Sec. 6).
+ *
+ * Conventions for every entry point:
+ *  - Argument structs are host memory.  Every pointer inside them is DEVICE
+ *    memory owned by the caller; the library keeps no reference after return.
+ *  - bf16 tensors are passed as raw 16-bit patterns (void*).
+ *  - All shape and flag validation happens on the host before any HIP call;
+ *    a rejected call launches nothing and returns MPFA_ERR_INVALID (bad
+ *    value, null pointer) or MPFA_ERR_UNSUPPORTED (valid but not built, e.g.
+ *    head_dim != 128).  Launch failures return MPFA_ERR_HIP.
+ *  - Work is enqueued asynchronously on `stream` (0 = default stream); no
+ *    host synchronisation and no device allocation happen inside
+ *    mpfa_prefill and mpfa_decode_paged, so both may be captured in a HIP
+ *    graph.  mpfa_quantize_qk does not allocate either.
+ *  - Data-dependent conditions (page index out of range, non-finite inputs,
+ *    kv_len larger than the page table) are NOT checked on the device: the
+ *    caller guarantees them.
+ *  - The library holds no mutable global state; concurrent calls on
+ *    different streams are safe when their output buffers do not overlap.
+ *
+ * Layouts (head_dim D = 128, 16-element NVFP4 groups, 64-token pages):
+ *  - Q, K, V inputs: bf16 [T][H][128], tokens of all sequences packed,
+ *    sequence b owning tokens cu_seqlens[b] .. cu_seqlens[b+1]-1.
+ *  - NVFP4 rows: 64 code bytes (channel 2i in the low nibble of byte i,
+ *    channel 2i+1 in the high nibble) + 8 E4M3 scale bytes (group g covers
+ *    channels 16g .. 16g+15) + one FP32 power-of-two tensor scale per
+ *    (sequence, head).  Value of channel c: t * e4m3(scale[c/16]) * e2m1(code).
+ *  - Paged cache, page p, KV head h, token slot o (0..63):
+ *      k_codes  u8   [P][H_kv][64][64]
+ *      k_scales u8   [P][H_kv][64][8]
+ *      v_codes  u8   [P][H_kv][128][64]   (channel-major: [channel][slot])
+ *      ds       bf16 [P][H_q][64]         (Delta_S side cache, smoothing only)
+ *    A token's slot is slot_mapping = page * 64 + o.
+ *  - page_table i32 [batch][max_pages]: logical page i of sequence b is
+ *    physical page page_table[b * max_pages + i]; key position j of the
+ *    sequence lives in logical page j / 64, slot j % 64.
+ *  - Query head h uses KV head h / (H_q / H_kv).
+ */
+#ifndef MPFA_H
+#define MPFA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* mpfa_stream_t;   /* == hipStream_t */
+
+typedef enum {
+    MPFA_OK = 0,
+    MPFA_ERR_INVALID = 1,      /* bad argument value or null pointer          */
+    MPFA_ERR_UNSUPPORTED = 2,  /* valid request this build does not implement */
+    MPFA_ERR_WORKSPACE = 3,    /* workspace missing or too small              */
+    MPFA_ERR_HIP = 4           /* a HIP launch or runtime call failed         */
+} mpfa_status;
+
+#define MPFA_HEAD_DIM 128
+#define MPFA_PAGE_TOKENS 64
+#define MPFA_KV_TILE 128
+#define MPFA_MAX_HEADS 256
+
+/* flags */
+#define MPFA_SMOOTH        1u  /* sequence centering + Delta_S compensation (off = "direct") */
+#define MPFA_COMPUTE_STATS 2u  /* compute means and K tensor scales from this call's tokens  */
+#define MPFA_TSCALE_UNIT   4u  /* NVFP4 tensor scale fixed to 1 (Eq. 1 without a 2nd level) */
+
+/* ------------------------------------------------------------------------ */
+/* Quantization / cache-write pass (Algorithm 1 stage one; Sec. 4.2, 4.3, 6) */
+/* ------------------------------------------------------------------------ */
+/*
+ * For each sequence b of the call:
+ *  - with MPFA_COMPUTE_STATS: Qbar, Kbar = per-(head, channel) means over the
+ *    call's tokens (Eq. 7), summed in FP32 sequentially inside 128-token
+ *    blocks and then over the block partials in order, divided in FP32 and
+ *    rounded to BF16 (written to q_mean / k_mean; zero without MPFA_SMOOTH);
+ *    k_tscale[b][h] = smallest 2^k (k in [-64, 64]) with 2688 * 2^k >= max
+ *    |K - Kbar| over the call's tokens (1 if that max is 0 or with
+ *    MPFA_TSCALE_UNIT).  Without the flag the means and k_tscale are read
+ *    (frozen after the first prefill, Sec. 6).
+ *  - q_tscale[b][h]: the same rule over this call's centered Q tokens.
+ *  - Q_c = Q - Qbar and K_c = K - Kbar in FP32; NVFP4 per 16-channel group:
+ *    scale = E4M3_RNE_sat(amax / (6 t)), codes = E2M1_RNE_sat(x / (t * scale))
+ *    with IEEE FP32 divisions; a group whose scale is 0 stores sign-only codes.
+ *  - V is stored as E4M3_RNE_sat(V) (no scale, not centered, Sec. 4.2).
+ *  - With MPFA_SMOOTH, ds[slot][h_q] = BF16_RNE(sum_c Qbar[h_q][c] * K_c[c])
+ *    as an FP32 fused multiply-add chain over c = 0..127 (Eq. 9).
+ * Writes q_codes/q_scales rows of this call's tokens and the cache slots given
+ * by slot_mapping.  Deterministic: identical inputs give identical bytes.
+ */
+typedef struct {
+    int32_t batch;            /* sequences in this call (>= 1)                    */
+    int32_t total_tokens;     /* T = cu_seqlens[batch] (host copy)               */
+    int32_t max_seqlen;       /* host: max tokens of one sequence in this call   */
+    int32_t h_q, h_kv;        /* heads; h_q % h_kv == 0, h_q <= MPFA_MAX_HEADS   */
+    int32_t head_dim;         /* must be 128                                     */
+    uint32_t flags;           /* MPFA_SMOOTH | MPFA_COMPUTE_STATS | MPFA_TSCALE_UNIT */
+    int64_t num_pages;        /* cache capacity in pages (slot_mapping < 64 * num_pages) */
+    const int32_t* cu_seqlens;   /* [batch+1]                                    */
+    const void* q;               /* bf16 [T][h_q][128]                           */
+    const void* k;               /* bf16 [T][h_kv][128]                          */
+    const void* v;               /* bf16 [T][h_kv][128]                          */
+    const int64_t* slot_mapping; /* [T]                                          */
+    void* q_mean;                /* bf16 [batch][h_q][128]   (out with STATS, else in) */
+    void* k_mean;                /* bf16 [batch][h_kv][128]  (out with STATS, else in) */
+    float* k_tscale;             /* [batch][h_kv]            (out with STATS, else in) */
+    uint8_t* q_codes;            /* out [T][h_q][64]                             */
+    uint8_t* q_scales;           /* out [T][h_q][8]                              */
+    float* q_tscale;             /* out [batch][h_q]                             */
+    uint8_t* k_codes;            /* cache, see layouts                           */
+    uint8_t* k_scales;
+    uint8_t* v_codes;
+    void* ds;                    /* bf16 cache; may be NULL without MPFA_SMOOTH  */
+} mpfa_quant_args;
+
+mpfa_status mpfa_quantize_qk(const mpfa_quant_args* args, mpfa_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Causal prefill (Algorithm 1 main loop; Sec. 5.1, 5.2)                      */
+/* ------------------------------------------------------------------------ */
+/*
+ * Query i of sequence b (token cu_seqlens[b] + i, absolute position
+ * q_start[b] + i) attends to keys 0 .. q_start[b] + i of the sequence's paged
+ * cache.  KV tiles of 128 keys (multiples of 128) are visited from the
+ * query's own tile down to tile 0.  For every tile:
+ *   S = 1 * Delta_S (rank-one seed, with MPFA_SMOOTH)
+ *       + dequant(Q_hat) dequant(K_hat)^T,  masked after the seed;
+ *   m' = max(m, rowmax S); P = 2^(lambda (S - m')), lambda = log2(e)/sqrt(128);
+ *   l = 2^(lambda (m - m')) l + rowsum P;  P_hat = E4M3(448 P);
+ *   O = 2^(lambda (m - m')) O + P_hat V_hat.
+ * Output out[token][h][:] = BF16(O / (448 l)).  Requires
+ * q_start[b] + (cu_seqlens[b+1] - cu_seqlens[b]) <= kv_len[b].
+ * The NVFP4 products are computed exactly (FP16 operands hold t-free
+ * scale * element values exactly); accumulation is FP32.
+ */
+typedef struct {
+    int32_t batch, h_q, h_kv, head_dim;
+    int32_t max_seqlen_q;     /* host: max query tokens of one sequence          */
+    int32_t max_pages;        /* page_table row length                           */
+    uint32_t flags;           /* MPFA_SMOOTH                                     */
+    const int32_t* cu_seqlens_q; /* [batch+1] query tokens                       */
+    const int32_t* q_start;   /* [batch] absolute position of query 0            */
+    const int32_t* kv_len;    /* [batch] keys in the cache (>= q_start + n_q)    */
+    const int32_t* page_table;/* [batch][max_pages]                              */
+    const uint8_t* q_codes;   /* [T][h_q][64]                                    */
+    const uint8_t* q_scales;  /* [T][h_q][8]                                     */
+    const float* q_tscale;    /* [batch][h_q]                                    */
+    const uint8_t* k_codes;
+    const uint8_t* k_scales;
+    const uint8_t* v_codes;
+    const void* ds;           /* bf16 side cache (MPFA_SMOOTH)                   */
+    const float* k_tscale;    /* [batch][h_kv]                                   */
+    void* out;                /* bf16 [T][h_q][128]                              */
+} mpfa_prefill_args;
+
+mpfa_status mpfa_prefill(const mpfa_prefill_args* args, mpfa_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Split-KV paged decode (Sec. 5.3, Sec. 6)                                   */
+/* ------------------------------------------------------------------------ */
+/*
+ * One query token per sequence (q rows indexed by sequence b), attending to
+ * all kv_len[b] keys (the new token included; it must already be in the
+ * cache).  Keys are split into partitions of partition_tokens keys
+ * ([p*P, (p+1)*P)); each partition is visited in 128-key tiles from last to
+ * first with its own (m, l, O), exactly as in prefill, and the partition
+ * states are merged by log-sum-exp:
+ *   M = max_p m_p; l = sum_p 2^(lambda (m_p - M)) l_p;
+ *   O = sum_p 2^(lambda (m_p - M)) O_p; out = BF16(O / (448 l)).
+ * The G = H_q / H_kv query heads of one KV head share one pass over the KV
+ * partition (GQA packing); the compensation becomes a rank-G seed.
+ * workspace: caller-owned device memory of at least
+ * mpfa_decode_workspace_size(...) bytes; its contents on entry are ignored.
+ */
+typedef struct {
+    int32_t batch, h_q, h_kv, head_dim;
+    int32_t max_pages;
+    int32_t partition_tokens; /* multiple of 128                                  */
+    int32_t max_partitions;   /* >= ceil(max_b kv_len[b] / partition_tokens)      */
+    uint32_t flags;           /* MPFA_SMOOTH                                      */
+    const int32_t* kv_len;    /* [batch], each >= 1                               */
+    const int32_t* page_table;/* [batch][max_pages]                               */
+    const uint8_t* q_codes;   /* [batch][h_q][64]                                 */
+    const uint8_t* q_scales;  /* [batch][h_q][8]                                  */
+    const float* q_tscale;    /* [batch][h_q]                                     */
+    const uint8_t* k_codes;
+    const uint8_t* k_scales;
+    const uint8_t* v_codes;
+    const void* ds;
+    const float* k_tscale;    /* [batch][h_kv]                                    */
+    void* out;                /* bf16 [batch][h_q][128]                           */
+} mpfa_decode_args;
+
+/* Bytes of decode workspace: batch * h_q * max_partitions * (128 + 2) * 4. */
+mpfa_status mpfa_decode_workspace_size(int32_t batch, int32_t h_q, int32_t max_partitions,
+                                       size_t* bytes);
+
+/* Host helper: choose partition_tokens (a multiple of 128) for a batch so
+ * that the number of (sequence, KV head, partition) work items is a few
+ * times the compute-unit count; kv_len_host is host memory [batch]. */
+mpfa_status mpfa_decode_choose_partition(int32_t batch, const int32_t* kv_len_host, int32_t h_kv,
+                                         int32_t num_cus, int32_t* partition_tokens);
+
+mpfa_status mpfa_decode_paged(const mpfa_decode_args* args, void* workspace, size_t workspace_bytes,
+                              mpfa_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Utilities                                                                  */
+/* ------------------------------------------------------------------------ */
+/* Element-wise device conversion used by the quantizer, exposed so that its
+ * rounding can be checked exhaustively: fmt 0 = FP32 -> E4M3 (RNE, saturating
+ * at 448, sign kept), fmt 1 = FP32 -> E2M1 (RNE, saturating at 6, sign kept,
+ * one code per output byte).  x and out are device pointers of n elements. */
+mpfa_status mpfa_convert(int32_t fmt, const float* x, int64_t n, uint8_t* out,
+                         mpfa_stream_t stream);
+
+const char* mpfa_status_string(mpfa_status status);
+
+/* Library version string (static storage). */
+const char* mpfa_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MPFA_H */

@@ -1,0 +1,209 @@
+"""MI355X-native QK4PV8 FlashAttention (MpFA): thin Python binding of libmpfa.so.
+
+Argument marshalling only: torch tensors provide device memory and the current
+stream; every step of the attention path runs in the library's HIP kernels.
+The binding raises if the compiled library is missing — there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "libmpfa.so")
+
+MPFA_OK, MPFA_ERR_INVALID, MPFA_ERR_UNSUPPORTED, MPFA_ERR_WORKSPACE, MPFA_ERR_HIP = range(5)
+SMOOTH, COMPUTE_STATS, TSCALE_UNIT = 1, 2, 4
+HEAD_DIM, PAGE, TILE = 128, 64, 128
+
+EXPORTED = ("mpfa_quantize_qk", "mpfa_prefill", "mpfa_decode_workspace_size",
+            "mpfa_decode_choose_partition", "mpfa_decode_paged", "mpfa_convert",
+            "mpfa_status_string", "mpfa_version")
+
+
+class MpfaError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+        self.status = status
+
+
+class QuantArgs(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("total_tokens", C.c_int32), ("max_seqlen", C.c_int32),
+                ("h_q", C.c_int32), ("h_kv", C.c_int32), ("head_dim", C.c_int32),
+                ("flags", C.c_uint32), ("num_pages", C.c_int64),
+                ("cu_seqlens", C.c_void_p), ("q", C.c_void_p), ("k", C.c_void_p),
+                ("v", C.c_void_p), ("slot_mapping", C.c_void_p), ("q_mean", C.c_void_p),
+                ("k_mean", C.c_void_p), ("k_tscale", C.c_void_p), ("q_codes", C.c_void_p),
+                ("q_scales", C.c_void_p), ("q_tscale", C.c_void_p), ("k_codes", C.c_void_p),
+                ("k_scales", C.c_void_p), ("v_codes", C.c_void_p), ("ds", C.c_void_p)]
+
+
+class PrefillArgs(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("h_q", C.c_int32), ("h_kv", C.c_int32),
+                ("head_dim", C.c_int32), ("max_seqlen_q", C.c_int32), ("max_pages", C.c_int32),
+                ("flags", C.c_uint32), ("cu_seqlens_q", C.c_void_p), ("q_start", C.c_void_p),
+                ("kv_len", C.c_void_p), ("page_table", C.c_void_p), ("q_codes", C.c_void_p),
+                ("q_scales", C.c_void_p), ("q_tscale", C.c_void_p), ("k_codes", C.c_void_p),
+                ("k_scales", C.c_void_p), ("v_codes", C.c_void_p), ("ds", C.c_void_p),
+                ("k_tscale", C.c_void_p), ("out", C.c_void_p)]
+
+
+class DecodeArgs(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("h_q", C.c_int32), ("h_kv", C.c_int32),
+                ("head_dim", C.c_int32), ("max_pages", C.c_int32),
+                ("partition_tokens", C.c_int32), ("max_partitions", C.c_int32),
+                ("flags", C.c_uint32), ("kv_len", C.c_void_p), ("page_table", C.c_void_p),
+                ("q_codes", C.c_void_p), ("q_scales", C.c_void_p), ("q_tscale", C.c_void_p),
+                ("k_codes", C.c_void_p), ("k_scales", C.c_void_p), ("v_codes", C.c_void_p),
+                ("ds", C.c_void_p), ("k_tscale", C.c_void_p), ("out", C.c_void_p)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libmpfa.so (built in-tree by build.py); raise if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run paper_2609_33135_amd/build.py")
+        L = C.CDLL(LIB_PATH)
+        L.mpfa_quantize_qk.restype = C.c_int
+        L.mpfa_quantize_qk.argtypes = [C.POINTER(QuantArgs), C.c_void_p]
+        L.mpfa_prefill.restype = C.c_int
+        L.mpfa_prefill.argtypes = [C.POINTER(PrefillArgs), C.c_void_p]
+        L.mpfa_decode_workspace_size.restype = C.c_int
+        L.mpfa_decode_workspace_size.argtypes = [C.c_int32, C.c_int32, C.c_int32,
+                                                 C.POINTER(C.c_size_t)]
+        L.mpfa_decode_choose_partition.restype = C.c_int
+        L.mpfa_decode_choose_partition.argtypes = [C.c_int32, C.c_void_p, C.c_int32, C.c_int32,
+                                                   C.POINTER(C.c_int32)]
+        L.mpfa_decode_paged.restype = C.c_int
+        L.mpfa_decode_paged.argtypes = [C.POINTER(DecodeArgs), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.mpfa_convert.restype = C.c_int
+        L.mpfa_convert.argtypes = [C.c_int32, C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p]
+        L.mpfa_status_string.restype = C.c_char_p
+        L.mpfa_status_string.argtypes = [C.c_int]
+        L.mpfa_version.restype = C.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(s: int) -> str:
+    return lib().mpfa_status_string(s).decode()
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _check(rc: int, what: str):
+    if rc != MPFA_OK:
+        raise MpfaError(rc, what)
+
+
+class PagedCache:
+    """Device buffers of the paged NVFP4/FP8 KV cache and the Delta_S side cache."""
+
+    def __init__(self, num_pages: int, h_q: int, h_kv: int, device="cuda", smooth=True):
+        import torch
+        self.num_pages, self.h_q, self.h_kv = num_pages, h_q, h_kv
+        u8 = dict(dtype=torch.uint8, device=device)
+        self.k_codes = torch.zeros((num_pages, h_kv, PAGE, 64), **u8)
+        self.k_scales = torch.zeros((num_pages, h_kv, PAGE, 8), **u8)
+        self.v_codes = torch.zeros((num_pages, h_kv, HEAD_DIM, PAGE), **u8)
+        self.ds = torch.zeros((num_pages, h_q, PAGE), dtype=torch.bfloat16, device=device) \
+            if smooth else None
+
+
+class SeqStats:
+    """Per-sequence statistics frozen after the first prefill (means, K tensor scale)."""
+
+    def __init__(self, batch: int, h_q: int, h_kv: int, device="cuda"):
+        import torch
+        self.q_mean = torch.zeros((batch, h_q, HEAD_DIM), dtype=torch.bfloat16, device=device)
+        self.k_mean = torch.zeros((batch, h_kv, HEAD_DIM), dtype=torch.bfloat16, device=device)
+        self.k_tscale = torch.ones((batch, h_kv), dtype=torch.float32, device=device)
+
+
+class QuantQ:
+    """NVFP4 queries of one call: codes [T][H][64], scales [T][H][8], tensor scale [B][H]."""
+
+    def __init__(self, total: int, batch: int, h_q: int, device="cuda"):
+        import torch
+        self.codes = torch.zeros((total, h_q, 64), dtype=torch.uint8, device=device)
+        self.scales = torch.zeros((total, h_q, 8), dtype=torch.uint8, device=device)
+        self.tscale = torch.zeros((batch, h_q), dtype=torch.float32, device=device)
+
+
+def quantize_qk(q, k, v, cu_seqlens, slot_mapping, cache: PagedCache, stats: SeqStats,
+                qout: QuantQ, flags: int, max_seqlen: int, stream=None):
+    """mpfa_quantize_qk: q bf16 [T][Hq][128], k/v bf16 [T][Hkv][128] on the device."""
+    T, h_q, d = q.shape
+    a = QuantArgs(batch=cu_seqlens.numel() - 1, total_tokens=T, max_seqlen=max_seqlen, h_q=h_q,
+                  h_kv=k.shape[1], head_dim=d, flags=flags, num_pages=cache.num_pages,
+                  cu_seqlens=_ptr(cu_seqlens), q=_ptr(q), k=_ptr(k), v=_ptr(v),
+                  slot_mapping=_ptr(slot_mapping), q_mean=_ptr(stats.q_mean),
+                  k_mean=_ptr(stats.k_mean), k_tscale=_ptr(stats.k_tscale),
+                  q_codes=_ptr(qout.codes), q_scales=_ptr(qout.scales),
+                  q_tscale=_ptr(qout.tscale), k_codes=_ptr(cache.k_codes),
+                  k_scales=_ptr(cache.k_scales), v_codes=_ptr(cache.v_codes), ds=_ptr(cache.ds))
+    _check(lib().mpfa_quantize_qk(C.byref(a), _stream(stream)), "mpfa_quantize_qk")
+
+
+def prefill(qq: QuantQ, cache: PagedCache, stats: SeqStats, cu_seqlens_q, q_start, kv_len,
+            page_table, out, max_seqlen_q: int, flags: int, stream=None):
+    """mpfa_prefill: causal attention of the quantized queries over the paged cache."""
+    a = PrefillArgs(batch=cu_seqlens_q.numel() - 1, h_q=qq.codes.shape[1], h_kv=cache.h_kv,
+                    head_dim=HEAD_DIM, max_seqlen_q=max_seqlen_q, max_pages=page_table.shape[1],
+                    flags=flags, cu_seqlens_q=_ptr(cu_seqlens_q), q_start=_ptr(q_start),
+                    kv_len=_ptr(kv_len), page_table=_ptr(page_table), q_codes=_ptr(qq.codes),
+                    q_scales=_ptr(qq.scales), q_tscale=_ptr(qq.tscale),
+                    k_codes=_ptr(cache.k_codes), k_scales=_ptr(cache.k_scales),
+                    v_codes=_ptr(cache.v_codes), ds=_ptr(cache.ds),
+                    k_tscale=_ptr(stats.k_tscale), out=_ptr(out))
+    _check(lib().mpfa_prefill(C.byref(a), _stream(stream)), "mpfa_prefill")
+
+
+def decode_workspace_size(batch: int, h_q: int, max_partitions: int) -> int:
+    n = C.c_size_t(0)
+    _check(lib().mpfa_decode_workspace_size(batch, h_q, max_partitions, C.byref(n)),
+           "mpfa_decode_workspace_size")
+    return n.value
+
+
+def decode_choose_partition(kv_len_host, h_kv: int, num_cus: int) -> int:
+    import numpy as np
+    kl = np.ascontiguousarray(kv_len_host, dtype=np.int32)
+    out = C.c_int32(0)
+    _check(lib().mpfa_decode_choose_partition(kl.size, kl.ctypes.data, h_kv, num_cus,
+                                              C.byref(out)), "mpfa_decode_choose_partition")
+    return out.value
+
+
+def decode_paged(qq: QuantQ, cache: PagedCache, stats: SeqStats, kv_len, page_table, out,
+                 partition_tokens: int, max_partitions: int, workspace, flags: int, stream=None):
+    """mpfa_decode_paged: one query per sequence (qq rows indexed by sequence)."""
+    a = DecodeArgs(batch=kv_len.numel(), h_q=qq.codes.shape[1], h_kv=cache.h_kv,
+                   head_dim=HEAD_DIM, max_pages=page_table.shape[1],
+                   partition_tokens=partition_tokens, max_partitions=max_partitions, flags=flags,
+                   kv_len=_ptr(kv_len), page_table=_ptr(page_table), q_codes=_ptr(qq.codes),
+                   q_scales=_ptr(qq.scales), q_tscale=_ptr(qq.tscale),
+                   k_codes=_ptr(cache.k_codes), k_scales=_ptr(cache.k_scales),
+                   v_codes=_ptr(cache.v_codes), ds=_ptr(cache.ds),
+                   k_tscale=_ptr(stats.k_tscale), out=_ptr(out))
+    _check(lib().mpfa_decode_paged(C.byref(a), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _stream(stream)),
+           "mpfa_decode_paged")
+
+
+def convert(fmt: int, x, out, stream=None):
+    """mpfa_convert: fmt 0 FP32 -> E4M3, fmt 1 FP32 -> E2M1 (one code per byte)."""
+    _check(lib().mpfa_convert(fmt, _ptr(x), x.numel(), _ptr(out), _stream(stream)), "mpfa_convert")

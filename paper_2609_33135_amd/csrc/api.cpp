@@ -1,0 +1,201 @@
+// api.cpp -- the C ABI of include/mpfa.h: host-side validation (no HIP call
+// before an argument set is accepted), launch configuration and the decode
+// partition policy.
+#include "mpfa.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "mpfa_internal.h"
+
+namespace {
+
+constexpr int kPrefillRows = 256;   // query rows per prefill workgroup
+constexpr int kMaxKvHeads = mpfa::kMaxKvHeadsQuant;
+constexpr int kMaxDecodeGroup = 8;  // query heads per KV head packed in one decode wave
+constexpr float kLambda = 0.12751743074173085f;   // log2(e) / sqrt(128)
+
+bool heads_ok(int h_q, int h_kv) {
+  return h_q >= 1 && h_kv >= 1 && h_q <= MPFA_MAX_HEADS && h_kv <= kMaxKvHeads && h_q % h_kv == 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mpfa_status_string(mpfa_status s) {
+  switch (s) {
+    case MPFA_OK: return "ok";
+    case MPFA_ERR_INVALID: return "invalid argument";
+    case MPFA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case MPFA_ERR_WORKSPACE: return "workspace missing or too small";
+    case MPFA_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* mpfa_version(void) { return "mpfa-gfx950 0.1"; }
+
+mpfa_status mpfa_quantize_qk(const mpfa_quant_args* a, mpfa_stream_t stream) {
+  if (!a) return MPFA_ERR_INVALID;
+  if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
+  if (a->batch < 1 || a->total_tokens < 0 || a->max_seqlen < 0 || a->num_pages < 1)
+    return MPFA_ERR_INVALID;
+  if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
+  if (a->flags & ~(MPFA_SMOOTH | MPFA_COMPUTE_STATS | MPFA_TSCALE_UNIT)) return MPFA_ERR_INVALID;
+  const bool smooth = a->flags & MPFA_SMOOTH;
+  if (!a->cu_seqlens || !a->q || !a->k || !a->v || !a->slot_mapping || !a->q_mean || !a->k_mean ||
+      !a->k_tscale || !a->q_codes || !a->q_scales || !a->q_tscale || !a->k_codes || !a->k_scales ||
+      !a->v_codes || (smooth && !a->ds))
+    return MPFA_ERR_INVALID;
+  if ((int64_t)a->batch * (a->h_q + a->h_kv) > INT32_MAX) return MPFA_ERR_INVALID;
+
+  mpfa::QuantParams p{};
+  p.batch = a->batch;
+  p.total_tokens = a->total_tokens;
+  p.h_q = a->h_q;
+  p.h_kv = a->h_kv;
+  p.smooth = smooth;
+  p.compute_stats = (a->flags & MPFA_COMPUTE_STATS) != 0;
+  p.stats_k = p.compute_stats;
+  p.tscale_unit = (a->flags & MPFA_TSCALE_UNIT) != 0;
+  p.cu_seqlens = a->cu_seqlens;
+  p.q = static_cast<const uint16_t*>(a->q);
+  p.k = static_cast<const uint16_t*>(a->k);
+  p.v = static_cast<const uint16_t*>(a->v);
+  p.slot_mapping = a->slot_mapping;
+  p.q_mean = static_cast<uint16_t*>(a->q_mean);
+  p.k_mean = static_cast<uint16_t*>(a->k_mean);
+  p.k_tscale = a->k_tscale;
+  p.q_codes = a->q_codes;
+  p.q_scales = a->q_scales;
+  p.q_tscale = a->q_tscale;
+  p.k_codes = a->k_codes;
+  p.k_scales = a->k_scales;
+  p.v_codes = a->v_codes;
+  p.ds = static_cast<uint16_t*>(a->ds);
+  return mpfa::launch_quantize(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
+                                                                                        : MPFA_ERR_HIP;
+}
+
+mpfa_status mpfa_prefill(const mpfa_prefill_args* a, mpfa_stream_t stream) {
+  if (!a) return MPFA_ERR_INVALID;
+  if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
+  if (a->batch < 1 || a->max_seqlen_q < 0 || a->max_pages < 1) return MPFA_ERR_INVALID;
+  if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
+  if (a->flags & ~MPFA_SMOOTH) return MPFA_ERR_INVALID;
+  const bool smooth = a->flags & MPFA_SMOOTH;
+  if (!a->cu_seqlens_q || !a->q_start || !a->kv_len || !a->page_table || !a->q_codes ||
+      !a->q_scales || !a->q_tscale || !a->k_codes || !a->k_scales || !a->v_codes ||
+      !a->k_tscale || !a->out || (smooth && !a->ds))
+    return MPFA_ERR_INVALID;
+  const int64_t n_qtiles = ((int64_t)a->max_seqlen_q + kPrefillRows - 1) / kPrefillRows;
+  if (n_qtiles * a->h_q * (int64_t)a->batch > INT32_MAX) return MPFA_ERR_INVALID;
+
+  mpfa::PrefillParams p{};
+  p.batch = a->batch;
+  p.h_q = a->h_q;
+  p.h_kv = a->h_kv;
+  p.max_pages = a->max_pages;
+  p.n_qtiles = (int)n_qtiles;
+  p.smooth = smooth;
+  p.xcd_remap = (a->h_kv % 8) == 0;
+  p.lam = kLambda;
+  p.cu_seqlens_q = a->cu_seqlens_q;
+  p.q_start = a->q_start;
+  p.kv_len = a->kv_len;
+  p.page_table = a->page_table;
+  p.q_codes = a->q_codes;
+  p.q_scales = a->q_scales;
+  p.q_tscale = a->q_tscale;
+  p.k_codes = a->k_codes;
+  p.k_scales = a->k_scales;
+  p.v_codes = a->v_codes;
+  p.ds = static_cast<const uint16_t*>(a->ds);
+  p.k_tscale = a->k_tscale;
+  p.out = static_cast<uint16_t*>(a->out);
+  return mpfa::launch_prefill(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
+                                                                                       : MPFA_ERR_HIP;
+}
+
+mpfa_status mpfa_decode_workspace_size(int32_t batch, int32_t h_q, int32_t max_partitions,
+                                       size_t* bytes) {
+  if (!bytes || batch < 1 || h_q < 1 || max_partitions < 1) return MPFA_ERR_INVALID;
+  *bytes = (size_t)batch * (size_t)h_q * (size_t)max_partitions * (MPFA_HEAD_DIM + 2) * sizeof(float);
+  return MPFA_OK;
+}
+
+mpfa_status mpfa_decode_choose_partition(int32_t batch, const int32_t* kv_len_host, int32_t h_kv,
+                                         int32_t num_cus, int32_t* partition_tokens) {
+  if (batch < 1 || !kv_len_host || h_kv < 1 || num_cus < 1 || !partition_tokens)
+    return MPFA_ERR_INVALID;
+  double total = 0.0;
+  for (int b = 0; b < batch; ++b) {
+    if (kv_len_host[b] < 1) return MPFA_ERR_INVALID;
+    total += (double)kv_len_host[b] * h_kv;
+  }
+  // aim for about 32 partition waves per compute unit
+  const double target_items = 32.0 * num_cus;
+  int64_t part = (int64_t)std::ceil(total / target_items / 128.0) * 128;
+  if (part < 256) part = 256;
+  if (part > 16384) part = 16384;
+  *partition_tokens = (int32_t)part;
+  return MPFA_OK;
+}
+
+mpfa_status mpfa_decode_paged(const mpfa_decode_args* a, void* workspace, size_t workspace_bytes,
+                              mpfa_stream_t stream) {
+  if (!a) return MPFA_ERR_INVALID;
+  if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
+  if (a->batch < 1 || a->batch > 65535 || a->max_pages < 1 || a->max_partitions < 1)
+    return MPFA_ERR_INVALID;
+  if (a->partition_tokens < MPFA_KV_TILE || a->partition_tokens % MPFA_KV_TILE)
+    return MPFA_ERR_INVALID;
+  if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
+  if (a->h_q / a->h_kv > kMaxDecodeGroup) return MPFA_ERR_UNSUPPORTED;
+  if (a->flags & ~MPFA_SMOOTH) return MPFA_ERR_INVALID;
+  const bool smooth = a->flags & MPFA_SMOOTH;
+  if (!a->kv_len || !a->page_table || !a->q_codes || !a->q_scales || !a->q_tscale ||
+      !a->k_codes || !a->k_scales || !a->v_codes || !a->k_tscale || !a->out || (smooth && !a->ds))
+    return MPFA_ERR_INVALID;
+  size_t need = 0;
+  if (mpfa_decode_workspace_size(a->batch, a->h_q, a->max_partitions, &need) != MPFA_OK)
+    return MPFA_ERR_INVALID;
+  if (!workspace || workspace_bytes < need) return MPFA_ERR_WORKSPACE;
+
+  mpfa::DecodeParams p{};
+  p.batch = a->batch;
+  p.h_q = a->h_q;
+  p.h_kv = a->h_kv;
+  p.max_pages = a->max_pages;
+  p.partition_tokens = a->partition_tokens;
+  p.max_partitions = a->max_partitions;
+  p.smooth = smooth;
+  p.lam = kLambda;
+  p.kv_len = a->kv_len;
+  p.page_table = a->page_table;
+  p.q_codes = a->q_codes;
+  p.q_scales = a->q_scales;
+  p.q_tscale = a->q_tscale;
+  p.k_codes = a->k_codes;
+  p.k_scales = a->k_scales;
+  p.v_codes = a->v_codes;
+  p.ds = static_cast<const uint16_t*>(a->ds);
+  p.k_tscale = a->k_tscale;
+  p.ws = static_cast<float*>(workspace);
+  p.out = static_cast<uint16_t*>(a->out);
+  return mpfa::launch_decode(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
+                                                                                      : MPFA_ERR_HIP;
+}
+
+mpfa_status mpfa_convert(int32_t fmt, const float* x, int64_t n, uint8_t* out, mpfa_stream_t stream) {
+  if ((fmt != 0 && fmt != 1) || n < 0 || (n > 0 && (!x || !out))) return MPFA_ERR_INVALID;
+  if (n > (int64_t)UINT32_MAX * 256) return MPFA_ERR_INVALID;
+  return mpfa::launch_convert(fmt, x, n, out, reinterpret_cast<hipStream_t>(stream)) == hipSuccess
+             ? MPFA_OK
+             : MPFA_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,165 @@
+// mpfa_device.h -- gfx950 device helpers for the QK4PV8 kernels: number-format
+// codecs written from the format definitions, exact NVFP4 dequantization into
+// FP16 MFMA operands, and thin wrappers over the CDNA4 matrix instructions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mpfa {
+
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kD = 128;        // head dimension
+constexpr int kPage = 64;      // tokens per cache page
+constexpr int kTile = 128;     // keys per KV tile
+constexpr float kLog2_448 = 8.807354922057604f;   // log2(448): P carries the fixed FP8 scale
+
+// ---------------------------------------------------------------------------
+// Number formats (Sec. 2.1 Eq. 1; Sec. 4.1)
+// ---------------------------------------------------------------------------
+
+// FP32 -> OCP E4M3 (bias 7, max 448), round to nearest even, saturating at 448,
+// sign kept.  Subnormal range (< 2^-6) is a fixed grid of 2^-9; above it the
+// 23-bit mantissa is rounded to 3 bits by the add-and-truncate rule with the
+// carry flowing into the exponent.
+__device__ __forceinline__ uint32_t e4m3_rne_sat(float x) {
+  uint32_t u = __float_as_uint(x);
+  uint32_t sign = (u >> 24) & 0x80u;
+  float a = __builtin_fabsf(x);
+  uint32_t code;
+  if (!(a < 448.0f)) {
+    code = 0x7Eu;
+  } else if (a < 0.015625f) {
+    code = (uint32_t)__builtin_rintf(a * 512.0f);
+  } else {
+    uint32_t ua = __float_as_uint(a);
+    uint32_t r = ua + 0x7FFFFu + ((ua >> 20) & 1u);
+    code = (r >> 20) - (120u << 3);
+  }
+  return sign | code;
+}
+
+// FP32 -> E2M1 (magnitudes 0, .5, 1, 1.5, 2, 3, 4, 6), round to nearest with
+// ties to the even code, saturating at 6, sign kept in bit 3.  The code is the
+// number of decision thresholds the magnitude passes; a tie sits on a
+// threshold and goes to the even side ('>' vs '>=').
+__device__ __forceinline__ uint32_t e2m1_rne_sat(float y) {
+  float a = __builtin_fabsf(y);
+  uint32_t c = (uint32_t)(a > 0.25f) + (uint32_t)(a >= 0.75f) + (uint32_t)(a > 1.25f) +
+               (uint32_t)(a >= 1.75f) + (uint32_t)(a > 2.5f) + (uint32_t)(a >= 3.5f) +
+               (uint32_t)(a > 5.0f);
+  return c | ((__float_as_uint(y) >> 28) & 8u);
+}
+
+// E4M3 code -> value (exact in FP32).
+__device__ __forceinline__ float e4m3_value(uint32_t c) {
+  uint32_t e = (c >> 3) & 15u, m = c & 7u;
+  float v = e ? __builtin_ldexpf(1.0f + (float)m * 0.125f, (int)e - 7) : (float)m * (1.0f / 512.0f);
+  return (c & 0x80u) ? -v : v;
+}
+
+// FP32 -> BF16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t bf16_rne(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// floor(log2 |x|) for finite nonzero x (v_frexp_exp returns it plus one).
+__device__ __forceinline__ int ilog2f(float x) { return __builtin_amdgcn_frexp_expf(x) - 1; }
+
+// Second-level NVFP4 scale: smallest 2^k, k in [-64, 64], with 2688 * 2^k >= amax
+// (so the largest group scale amax / (6 t) is at most 448); 1 when amax == 0.
+__device__ __forceinline__ float tensor_scale(float amax) {
+  if (!(amax > 0.0f)) return 1.0f;
+  int e = ilog2f(amax);                    // amax in [2^e, 2^(e+1))
+  int k = e - 12;
+  while (k < 64 && __builtin_ldexpf(2688.0f, k) < amax) ++k;
+  while (k > -64 && __builtin_ldexpf(2688.0f, k - 1) >= amax) --k;
+  if (k < -64) k = -64;
+  if (k > 64) k = 64;
+  return __builtin_ldexpf(1.0f, k);
+}
+
+// ---------------------------------------------------------------------------
+// Exact NVFP4 -> FP16 dequantization.
+// An E4M3 scale s = 2^E * M splits into a power of two (E in [-6, 8]) and a
+// mantissa M = 1 + m/8 (normal) or m/8 (subnormal).  v_cvt_scalef32_pk_f16_fp4
+// applies only the exponent of its scale operand, giving q * 2^E exactly; one
+// packed FP16 multiply by M then yields s * q exactly (at most 6 significant
+// bits, magnitude in [2^-10, 2688]: always an FP16 normal number).
+// ---------------------------------------------------------------------------
+struct ScaleSplit {
+  float pow2;     // 2^E
+  f16x2 mant;     // (M, M)
+};
+
+__device__ __forceinline__ ScaleSplit split_e4m3(uint32_t code) {
+  uint32_t e = (code >> 3) & 15u, m = code & 7u;
+  ScaleSplit s;
+  if (e) {
+    s.pow2 = __builtin_ldexpf(1.0f, (int)e - 7);
+    _Float16 mm = (_Float16)(1.0f + (float)m * 0.125f);
+    s.mant = (f16x2){mm, mm};
+  } else {
+    s.pow2 = 0.015625f;   // 2^-6
+    _Float16 mm = (_Float16)((float)m * 0.125f);
+    s.mant = (f16x2){mm, mm};
+  }
+  return s;
+}
+
+// Eight E2M1 codes (one dword, channel order low nibble first) -> eight FP16.
+__device__ __forceinline__ f16x8 dequant8(uint32_t codes, ScaleSplit s) {
+  f16x2 a = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, s.pow2, 0) * s.mant;
+  f16x2 b = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, s.pow2, 1) * s.mant;
+  f16x2 c = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, s.pow2, 2) * s.mant;
+  f16x2 d = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, s.pow2, 3) * s.mant;
+  return (f16x8){a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
+}
+
+// ---------------------------------------------------------------------------
+// Matrix instructions (16x16 output tiles, 64-lane wavefront).
+// Operand layout (verified on gfx950): lane l supplies row (A) / column (B)
+// l % 16 and a contiguous slice of the reduction dimension selected by l / 16;
+// the accumulator lane l holds rows 4*(l/16) .. 4*(l/16)+3 of column l % 16.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ f32x4 mfma_f16(f16x8 a, f16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+// FP8 E4M3 x FP8 E4M3, K = 128, unit block scales (E8M0 127 = 2^0).
+__device__ __forceinline__ f32x4 mfma_fp8(i32x8 a, i32x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0x7F7F7F7F, 0, 0x7F7F7F7F);
+}
+
+// Four FP32 values in [0, 448] -> four E4M3 bytes (hardware RNE).
+__device__ __forceinline__ uint32_t pack_fp8x4(float a, float b, float c, float d) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
+  return (uint32_t)w;
+}
+
+__device__ __forceinline__ float wave_max16(float x) {
+  x = fmaxf(x, __shfl_xor(x, 16));
+  x = fmaxf(x, __shfl_xor(x, 32));
+  return x;
+}
+__device__ __forceinline__ float wave_sum16(float x) {
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+
+}  // namespace mpfa

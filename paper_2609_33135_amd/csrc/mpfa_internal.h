@@ -1,0 +1,77 @@
+// mpfa_internal.h -- launch parameter blocks shared by the host API layer and
+// the gfx950 kernels.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mpfa {
+
+constexpr int kMaxKvHeadsQuant = 32;
+
+struct QuantParams {
+  int batch, total_tokens, h_q, h_kv;
+  int smooth, compute_stats, stats_k, tscale_unit;
+  const int32_t* cu_seqlens;
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int64_t* slot_mapping;
+  uint16_t* q_mean;
+  uint16_t* k_mean;
+  float* k_tscale;
+  uint8_t* q_codes;
+  uint8_t* q_scales;
+  float* q_tscale;
+  uint8_t* k_codes;
+  uint8_t* k_scales;
+  uint8_t* v_codes;
+  uint16_t* ds;
+};
+
+struct PrefillParams {
+  int batch, h_q, h_kv, max_pages;
+  int n_qtiles;     // max query tiles of one sequence
+  int smooth;
+  int xcd_remap;    // 1: spread KV heads over the 8 XCDs (needs h_kv % 8 == 0)
+  float lam;        // log2(e) / sqrt(128)
+  const int32_t* cu_seqlens_q;
+  const int32_t* q_start;
+  const int32_t* kv_len;
+  const int32_t* page_table;
+  const uint8_t* q_codes;
+  const uint8_t* q_scales;
+  const float* q_tscale;
+  const uint8_t* k_codes;
+  const uint8_t* k_scales;
+  const uint8_t* v_codes;
+  const uint16_t* ds;
+  const float* k_tscale;
+  uint16_t* out;
+};
+
+struct DecodeParams {
+  int batch, h_q, h_kv, max_pages;
+  int partition_tokens, max_partitions;
+  int smooth;
+  float lam;
+  const int32_t* kv_len;
+  const int32_t* page_table;
+  const uint8_t* q_codes;
+  const uint8_t* q_scales;
+  const float* q_tscale;
+  const uint8_t* k_codes;
+  const uint8_t* k_scales;
+  const uint8_t* v_codes;
+  const uint16_t* ds;
+  const float* k_tscale;
+  float* ws;        // [batch][h_q][max_partitions][130]: m*lambda', l, O[128]
+  uint16_t* out;
+};
+
+hipError_t launch_quantize(const QuantParams& p, hipStream_t stream);
+hipError_t launch_convert(int fmt, const float* x, int64_t n, uint8_t* out, hipStream_t stream);
+hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);
+hipError_t launch_decode(const DecodeParams& p, hipStream_t stream);
+
+}  // namespace mpfa

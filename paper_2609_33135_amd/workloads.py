@@ -191,3 +191,45 @@ def mixed_step(n_decode: int = 64) -> tuple:
     dec = DecodeWorkload(f"qwen3-14b-shaped paged decode, batch {n_decode}, contexts U[8192,131072]",
                          n_decode, 40, 8, draw_lengths(55, n_decode, 8192, 131072), seed=55)
     return pre, dec
+
+
+def gen_qkv(seed, seqlens, h_q, h_kv, outliers, device, tok_offsets=None, seq_ids=None):
+    """Concatenated bf16 Q, K, V for sequences of the given lengths.  Entry i is
+    sequence seq_ids[i] (default i) of the seeded stream, starting at its token
+    tok_offsets[i] (default 0)."""
+    qs, ks, vs = [], [], []
+    off = k_offsets(seed, h_kv, device=device)
+    for i, n in enumerate(seqlens):
+        b = i if seq_ids is None else int(seq_ids[i])
+        t0 = 0 if tok_offsets is None else int(tok_offsets[i])
+        qs.append(gen_tensor(seed, STREAM_Q, b, t0, n, h_q, device, outliers, STREAM_OUT_Q))
+        ks.append(gen_tensor(seed, STREAM_K, b, t0, n, h_kv, device, outliers, STREAM_OUT_K,
+                             offset=off))
+        vs.append(gen_tensor(seed, STREAM_V, b, t0, n, h_kv, device))
+    return torch.cat(qs), torch.cat(ks), torch.cat(vs)
+
+
+def make_pages(seed, kv_lens, shuffle=True):
+    """Page table [B][max_pages] over a shared pool of 64-token pages, physical
+    pages permuted.  Returns (page_table int32, pages used)."""
+    need = [(int(n) + 63) // 64 for n in kv_lens]
+    total = int(sum(need))
+    perm = page_permutation(seed, total) if shuffle else np.arange(total, dtype=np.int32)
+    maxp = max(need) if need else 1
+    pt = np.zeros((len(kv_lens), max(maxp, 1)), np.int32)
+    i = 0
+    for b, n in enumerate(need):
+        pt[b, :n] = perm[i:i + n]
+        i += n
+    return pt, total
+
+
+def slots_for(page_table, b, positions):
+    """Cache slots (page * 64 + offset) of key positions of sequence b."""
+    positions = np.asarray(positions, np.int64)
+    return page_table[b, positions // 64].astype(np.int64) * 64 + positions % 64
+
+
+def bits(t: torch.Tensor) -> np.ndarray:
+    """bf16 tensor -> uint16 numpy bit patterns (CPU copy)."""
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)

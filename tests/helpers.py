@@ -1,0 +1,118 @@
+"""Helpers shared by the GPU parity tests: build seeded workloads, run the HIP
+path through the C ABI and the CPU oracle on the same input bits, compare."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from paper_2609_33135_amd import workloads as W
+
+TOL_MAX_ABS = 1e-2      # bf16 vs bf16, element-wise
+TOL_MEAN_REL = 1e-3     # sum |a - b| / sum |b|
+
+
+def bf16_f64(b: np.ndarray) -> np.ndarray:
+    return (np.asarray(b, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+gen_qkv = W.gen_qkv
+make_pages = W.make_pages
+slots_for = W.slots_for
+bits = W.bits
+
+
+def bf16_ulp(x: np.ndarray) -> np.ndarray:
+    """Spacing of BF16 values at |x| (8 significant bits)."""
+    ax = np.maximum(np.abs(x), 2.0 ** -126)
+    return 2.0 ** (np.floor(np.log2(ax)) - 7)
+
+
+def compare_bf16(got_bits, ref_bits, what=""):
+    """Element-wise bar: |a - b| <= 1e-2, or at most one BF16 unit in the last
+    place of the larger magnitude (outputs above 2 have a BF16 spacing of
+    2^-6 > 1e-2, so one rounding step is the finest difference the format can
+    express there).  Returns (max |a - b| over elements, mean relative error,
+    number of elements failing the bar)."""
+    a = bf16_f64(got_bits)
+    b = bf16_f64(ref_bits)
+    diff = np.abs(a - b)
+    max_abs = float(diff.max()) if diff.size else 0.0
+    mean_rel = float(diff.sum() / max(np.abs(b).sum(), 1e-30))
+    allow = np.maximum(TOL_MAX_ABS, bf16_ulp(np.maximum(np.abs(a), np.abs(b))))
+    n_bad = int((diff > allow).sum())
+    return max_abs, mean_rel, n_bad
+
+
+class Run:
+    """One quantize (+ optional prefill) through the HIP path and the oracle."""
+
+    def __init__(self, orc, mp, seed, seqlens, h_q, h_kv, outliers=True, smooth=True,
+                 tscale_unit=False, shuffle=True, device="cuda"):
+        self.orc, self.mp = orc, mp
+        self.seqlens = list(seqlens)
+        self.h_q, self.h_kv = h_q, h_kv
+        self.smooth = smooth
+        B = len(seqlens)
+        self.B = B
+        q, k, v = gen_qkv(seed, seqlens, h_q, h_kv, outliers, device)
+        self.q, self.k, self.v = q, k, v
+        cu = np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32)
+        self.cu = cu
+        self.pt, self.n_pages = make_pages(seed, seqlens, shuffle)
+        slots = np.concatenate([slots_for(self.pt, b, np.arange(n)) for b, n in enumerate(seqlens)]) \
+            if cu[-1] > 0 else np.zeros(0, np.int64)
+        self.slots = slots
+        flags = (mp.SMOOTH if smooth else 0) | mp.COMPUTE_STATS | (mp.TSCALE_UNIT if tscale_unit else 0)
+        self.flags = flags
+        # HIP path
+        T = int(cu[-1])
+        self.cache = mp.PagedCache(max(self.n_pages, 1), h_q, h_kv, device, smooth=True)
+        self.stats = mp.SeqStats(B, h_q, h_kv, device)
+        self.qq = mp.QuantQ(T, B, h_q, device)
+        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+        self.cu_d = dev(cu)
+        self.slots_d = dev(slots)
+        mp.quantize_qk(q, k, v, self.cu_d, self.slots_d, self.cache, self.stats, self.qq, flags,
+                       max(seqlens) if seqlens else 0)
+        torch.cuda.synchronize()
+        # oracle on the same bits
+        self.ref = orc.quantize_qk(bits(q), bits(k), bits(v), cu, slots, max(self.n_pages, 1),
+                                   (orc.SMOOTH if smooth else 0) | orc.COMPUTE_STATS |
+                                   (orc.TSCALE_UNIT if tscale_unit else 0))
+
+    def gpu_quant(self):
+        c = self.cache
+        out = dict(q_codes=self.qq.codes, q_scales=self.qq.scales, q_tscale=self.qq.tscale,
+                   q_mean=self.stats.q_mean, k_mean=self.stats.k_mean,
+                   k_tscale=self.stats.k_tscale, k_codes=c.k_codes, k_scales=c.k_scales,
+                   v_codes=c.v_codes, ds=c.ds)
+        res = {}
+        for k_, t in out.items():
+            if t.dtype == torch.bfloat16:
+                res[k_] = bits(t)
+            else:
+                res[k_] = t.detach().cpu().numpy()
+        return res
+
+    def prefill_gpu(self, q_start=None, kv_len=None):
+        mp = self.mp
+        B = self.B
+        q_start = np.zeros(B, np.int32) if q_start is None else np.asarray(q_start, np.int32)
+        kv_len = np.asarray(self.seqlens if kv_len is None else kv_len, np.int32)
+        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+        T = int(self.cu[-1])
+        out = torch.full((T, self.h_q, 128), float("nan"), dtype=torch.bfloat16, device="cuda")
+        mp.prefill(self.qq, self.cache, self.stats, self.cu_d, dev(q_start), dev(kv_len),
+                   dev(self.pt), out, max(self.seqlens), mp.SMOOTH if self.smooth else 0)
+        torch.cuda.synchronize()
+        return bits(out)
+
+    def prefill_oracle(self, items, q_start=None, kv_len=None):
+        B = self.B
+        q_start = np.zeros(B, np.int32) if q_start is None else np.asarray(q_start, np.int32)
+        kv_len = np.asarray(self.seqlens if kv_len is None else kv_len, np.int32)
+        r = self.ref
+        o16, o64 = self.orc.prefill(r["cache"], self.pt, kv_len, r["k_tscale"], r["q_codes"],
+                                    r["q_scales"], r["q_tscale"], self.cu, q_start, items,
+                                    smooth=self.smooth)
+        return o16, o64

@@ -1,0 +1,134 @@
+"""The C-ABI library loads without a GPU, exports every entry point declared in
+include/*.h, and rejects bad arguments on the host before any HIP call."""
+import ctypes as C
+import glob
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(mpfa_[a-z0-9_]+)\s*\(", text))
+    return names
+
+
+@pytest.fixture(scope="module")
+def mp():
+    import paper_2609_33135_amd as mp
+    if not os.path.exists(mp.LIB_PATH):
+        from paper_2609_33135_amd import build
+        build.build()
+    mp.lib()
+    return mp
+
+
+def test_exports_every_declared_symbol(mp):
+    names = _declared()
+    assert {"mpfa_quantize_qk", "mpfa_prefill", "mpfa_decode_paged"} <= names
+    L = C.CDLL(mp.LIB_PATH)
+    for n in sorted(names):
+        assert hasattr(L, n), f"{n} declared in include/ but not exported"
+    assert set(mp.EXPORTED) == names
+
+
+def test_status_strings(mp):
+    for s in range(5):
+        assert mp.status_string(s)
+    assert mp.lib().mpfa_version().decode().startswith("mpfa")
+
+
+def _prefill_args(mp, **kw):
+    a = mp.PrefillArgs(batch=1, h_q=8, h_kv=2, head_dim=128, max_seqlen_q=16, max_pages=1, flags=1)
+    for f in ("cu_seqlens_q", "q_start", "kv_len", "page_table", "q_codes", "q_scales", "q_tscale",
+              "k_codes", "k_scales", "v_codes", "ds", "k_tscale", "out"):
+        setattr(a, f, 0x1000)   # never dereferenced: validation fails before any launch
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 64, 2), ("head_dim", 0, 1), ("h_q", 7, 1), ("h_kv", 0, 1), ("batch", 0, 1),
+    ("max_pages", 0, 1), ("flags", 8, 1), ("q_codes", None, 1), ("ds", None, 1),
+    ("max_seqlen_q", -1, 1), ("h_kv", 64, 1),
+])
+def test_prefill_validation(mp, field, value, status):
+    a = _prefill_args(mp, **{field: value})
+    assert mp.lib().mpfa_prefill(C.byref(a), None) == status
+
+
+def test_prefill_direct_needs_no_side_cache(mp):
+    # without MPFA_SMOOTH a null ds is accepted by validation; use an invalid
+    # head count as well so that nothing is launched
+    a = _prefill_args(mp, flags=0, ds=None, h_q=7)
+    assert mp.lib().mpfa_prefill(C.byref(a), None) == 1
+
+
+def _decode_args(mp, **kw):
+    a = mp.DecodeArgs(batch=2, h_q=32, h_kv=8, head_dim=128, max_pages=4, partition_tokens=256,
+                      max_partitions=2, flags=1)
+    for f in ("kv_len", "page_table", "q_codes", "q_scales", "q_tscale", "k_codes", "k_scales",
+              "v_codes", "ds", "k_tscale", "out"):
+        setattr(a, f, 0x1000)
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("partition_tokens", 100, 1), ("partition_tokens", 0, 1), ("max_partitions", 0, 1),
+    ("h_q", 72, 2), ("head_dim", 256, 2), ("kv_len", None, 1), ("flags", 2, 1),
+])
+def test_decode_validation(mp, field, value, status):
+    a = _decode_args(mp, **{field: value})
+    assert mp.lib().mpfa_decode_paged(C.byref(a), 0x1000, 1 << 40, None) == status
+
+
+def test_decode_workspace_checks(mp):
+    a = _decode_args(mp)
+    need = mp.decode_workspace_size(2, 32, 2)
+    assert need == 2 * 32 * 2 * 130 * 4
+    assert mp.lib().mpfa_decode_paged(C.byref(a), None, need, None) == 3
+    assert mp.lib().mpfa_decode_paged(C.byref(a), 0x1000, need - 1, None) == 3
+
+
+def test_choose_partition(mp):
+    lens = np.array([16384, 131072, 50000, 8000] * 8, np.int32)
+    p = mp.decode_choose_partition(lens, 8, 256)
+    assert p % 128 == 0 and 256 <= p <= 16384
+    items = sum(-(-int(n) // p) for n in lens) * 8
+    assert items >= 256          # enough partition waves to cover the chip
+    with pytest.raises(mp.MpfaError):
+        mp.decode_choose_partition(np.array([0], np.int32), 8, 256)
+
+
+def test_quantize_validation(mp):
+    a = mp.QuantArgs(batch=1, total_tokens=4, max_seqlen=4, h_q=4, h_kv=2, head_dim=128, flags=3,
+                     num_pages=1)
+    for f in ("cu_seqlens", "q", "k", "v", "slot_mapping", "q_mean", "k_mean", "k_tscale",
+              "q_codes", "q_scales", "q_tscale", "k_codes", "k_scales", "v_codes", "ds"):
+        setattr(a, f, 0x1000)
+    a.ds = None
+    assert mp.lib().mpfa_quantize_qk(C.byref(a), None) == 1      # smoothing needs the side cache
+    a.ds = 0x1000
+    a.flags = 16
+    assert mp.lib().mpfa_quantize_qk(C.byref(a), None) == 1
+    a.flags = 3
+    a.head_dim = 96
+    assert mp.lib().mpfa_quantize_qk(C.byref(a), None) == 2
+    a.head_dim = 128
+    a.h_kv = 3
+    assert mp.lib().mpfa_quantize_qk(C.byref(a), None) == 1
+
+
+def test_convert_validation(mp):
+    assert mp.lib().mpfa_convert(2, None, 0, None, None) == 1
+    assert mp.lib().mpfa_convert(0, None, 5, None, None) == 1
