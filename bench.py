@@ -44,7 +44,9 @@ def parse():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-direct", action="store_true", help="skip the unsmoothed prefill variant")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=4096, help="oracle sample: query rows of head 0")
+    ap.add_argument("--cpu-rows", type=int, default=16384, help="oracle sample: query rows of head 0")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (reference for memory counters)")
     return ap.parse_args()
 
 
@@ -226,6 +228,18 @@ def main():
                                         "path peak (FP16 QK + FP8 PV) is "
                                         f"{flops / (f_qk / PEAK_BF16 + f_pv / PEAK_FP8) / 1e12:.0f}"}
         if not args.no_direct:
+            log("prefill with the compensation loaded as accumulator input ...")
+            st["flags"] = mp.SMOOTH | mp.SEED_INIT
+            for _ in range(args.warmup):
+                run_prefill(mp, st)
+            ts = []
+            for _ in range(args.steps):
+                with Timer(torch) as t2:
+                    run_prefill(mp, st)
+                ts.append(t2)
+            torch.cuda.synchronize()
+            res["prefill"]["seed_init_ms"] = sum(t.ms() for t in ts) / args.steps
+            st["flags"] = mp.SMOOTH
             log("prefill direct (unsmoothed) variant ...")
             del st["cache"]
             std = setup_prefill(torch, np, mp, W, seq, smooth=False)
@@ -266,6 +280,14 @@ def main():
         res["decode"] = {"ms": decode_ms, "GB/s": gbs, "frac_hbm": gbs * 1e9 / PEAK_HBM,
                          "bytes": nbytes, "partition_tokens": sd["part"],
                          "keys": int(sum(sd["lens"]))}
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        res["copy_calibration_bytes"] = 1 << 30
 
     line = {
         "metric": "prefill attn TFLOPS (causal 128K) + decode KV GB/s, % of roofline, 1 MI355X",

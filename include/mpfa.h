@@ -76,6 +76,9 @@ typedef enum {
 #define MPFA_SMOOTH        1u  /* sequence centering + Delta_S compensation (off = "direct") */
 #define MPFA_COMPUTE_STATS 2u  /* compute means and K tensor scales from this call's tokens  */
 #define MPFA_TSCALE_UNIT   4u  /* NVFP4 tensor scale fixed to 1 (Eq. 1 without a 2nd level) */
+#define MPFA_SEED_INIT     8u  /* prefill: load the rank-one term 1 Delta_S^T as the input
+                                  accumulator of the first QK MFMA instead of issuing the
+                                  BF16 rank-one MFMA; results are bit-identical            */
 
 /* ------------------------------------------------------------------------ */
 /* Quantization / cache-write pass (Algorithm 1 stage one; Sec. 4.2, 4.3, 6) */
@@ -149,7 +152,7 @@ typedef struct {
     int32_t batch, h_q, h_kv, head_dim;
     int32_t max_seqlen_q;     /* host: max query tokens of one sequence          */
     int32_t max_pages;        /* page_table row length                           */
-    uint32_t flags;           /* MPFA_SMOOTH                                     */
+    uint32_t flags;           /* MPFA_SMOOTH, MPFA_SEED_INIT                     */
     const int32_t* cu_seqlens_q; /* [batch+1] query tokens                       */
     const int32_t* q_start;   /* [batch] absolute position of query 0            */
     const int32_t* kv_len;    /* [batch] keys in the cache (>= q_start + n_q)    */

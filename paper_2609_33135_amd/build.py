@@ -15,6 +15,7 @@ LIB = os.path.join(PKG, "libmpfa.so")
 
 SOURCES = ["api.cpp", "quantize.hip", "prefill.hip", "decode.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+CLANG = os.environ.get("MPFA_CLANG", "/opt/rocm/lib/llvm/bin/clang++")
 ARCH = os.environ.get("MPFA_ARCH", "gfx950")
 
 COMMON = [
@@ -27,9 +28,7 @@ COMMON = [
 
 def _compile(src: str) -> str:
     out = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *COMMON, "-c", os.path.join(CSRC, src), "-o", out]
-    if src.endswith(".cpp"):
-        cmd[1:1] = ["-x", "hip"]
+    cmd = [CLANG, "-x", "hip", *COMMON, "-c", os.path.join(CSRC, src), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
     msg = "\n".join(l for l in (r.stdout + r.stderr).splitlines() if noise not in l)

@@ -104,17 +104,12 @@ struct ScaleSplit {
 };
 
 __device__ __forceinline__ ScaleSplit split_e4m3(uint32_t code) {
-  uint32_t e = (code >> 3) & 15u, m = code & 7u;
+  const uint32_t e = (code >> 3) & 15u, m = code & 7u;
   ScaleSplit s;
-  if (e) {
-    s.pow2 = __builtin_ldexpf(1.0f, (int)e - 7);
-    _Float16 mm = (_Float16)(1.0f + (float)m * 0.125f);
-    s.mant = (f16x2){mm, mm};
-  } else {
-    s.pow2 = 0.015625f;   // 2^-6
-    _Float16 mm = (_Float16)((float)m * 0.125f);
-    s.mant = (f16x2){mm, mm};
-  }
+  // subnormal codes (e == 0) share the exponent of e == 1 without the implicit 1
+  s.pow2 = __uint_as_float((uint32_t)(max(e, 1u) + 120u) << 23);   // 2^(max(e,1) - 7)
+  const _Float16 mm = (_Float16)((float)((e ? 8u : 0u) + m) * 0.125f);
+  s.mant = (f16x2){mm, mm};
   return s;
 }
 

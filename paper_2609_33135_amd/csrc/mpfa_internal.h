@@ -33,6 +33,7 @@ struct PrefillParams {
   int batch, h_q, h_kv, max_pages;
   int n_qtiles;     // max query tiles of one sequence
   int smooth;
+  int seed_init;    // 1: compensation loaded as the accumulator input, 0: rank-one MFMA
   int xcd_remap;    // 1: spread KV heads over the 8 XCDs (needs h_kv % 8 == 0)
   float lam;        // log2(e) / sqrt(128)
   const int32_t* cu_seqlens_q;

@@ -51,63 +51,95 @@ __device__ __forceinline__ u32x4 zero_tail(u32x4 w, int nvalid) {
   return w;
 }
 
-__device__ __forceinline__ void load_tile(PrefillSmem& sm, const PrefillParams& p, int b, int hk,
-                                          int h, int j, int kvl, float seed_scale) {
+// Raw bytes of one KV tile held in registers between the global load and the
+// LDS store (software pipelining: the next tile is fetched while the current
+// one is computed).
+struct TileRegs {
+  u32x4 kc;        // 16 NVFP4 code bytes: key t/4, channels 32*(t%4) .. +31
+  uint32_t ksc;    // their two E4M3 group scales
+  u32x4 v0, v1;    // 32 FP8 bytes: channel t/4, keys 32*(t%4) .. +31 of the tile
+  uint32_t ds;     // BF16 Delta_S of key t (threads 0..127)
+};
+
+__device__ __forceinline__ void fetch_tile(TileRegs& r, const PrefillParams& p, const int32_t* pt,
+                                           int hk, int h, int j, int kvl) {
   const int t = threadIdx.x;
-  const int32_t* pt = p.page_table + (int64_t)b * p.max_pages;
-  {  // K: 4 threads per key, 32 channels each
+  // the two pages of tile j: uniform across the workgroup (scalar loads)
+  const int npg = (kvl + 63) >> 6;
+  const int64_t pg0 = pt[min(2 * j, npg - 1)];
+  const int64_t pg1 = pt[min(2 * j + 1, npg - 1)];
+  {
     const int key = t >> 2, qt = t & 3;
     const int kabs = j * kTile + key;
-    u32x4 codes = {0u, 0u, 0u, 0u};
-    uint32_t sc = 0;
+    const int64_t row = ((key < 64 ? pg0 : pg1) * p.h_kv + hk) * kPage + (kabs & 63);
+    r.kc = (u32x4){0u, 0u, 0u, 0u};
+    r.ksc = 0;
     if (kabs < kvl) {
-      const int64_t page = pt[kabs >> 6];
-      const int64_t row = (page * p.h_kv + hk) * kPage + (kabs & 63);
-      codes = *reinterpret_cast<const u32x4*>(p.k_codes + row * 64 + qt * 16);
-      sc = *reinterpret_cast<const uint16_t*>(p.k_scales + row * 8 + qt * 2);
+      r.kc = *reinterpret_cast<const u32x4*>(p.k_codes + row * 64 + qt * 16);
+      r.ksc = *reinterpret_cast<const uint16_t*>(p.k_scales + row * 8 + qt * 2);
     }
-    const ScaleSplit s0 = split_e4m3(sc & 0xFFu), s1 = split_e4m3((sc >> 8) & 0xFFu);
-    uint8_t* rowp = sm.k + key * 256;
-    const int sw = k_swz(key);
-    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 0) ^ sw) << 4)) = dequant8(codes[0], s0);
-    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 1) ^ sw) << 4)) = dequant8(codes[1], s0);
-    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 2) ^ sw) << 4)) = dequant8(codes[2], s1);
-    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 3) ^ sw) << 4)) = dequant8(codes[3], s1);
   }
-  {  // V: 4 threads per channel, 32 keys each
+  {
     const int d = t >> 2, part = t & 3;
     const int kbase = j * kTile + part * 32;
-    u32x4 v0 = {0u, 0u, 0u, 0u}, v1 = {0u, 0u, 0u, 0u};
+    r.v0 = (u32x4){0u, 0u, 0u, 0u};
+    r.v1 = (u32x4){0u, 0u, 0u, 0u};
     if (kbase < kvl) {
-      const int64_t page = pt[kbase >> 6];
-      const uint8_t* src = p.v_codes + ((page * p.h_kv + hk) * kD + d) * kPage + (kbase & 63);
-      v0 = *reinterpret_cast<const u32x4*>(src);
-      v1 = *reinterpret_cast<const u32x4*>(src + 16);
+      const uint8_t* src = p.v_codes + (((part < 2 ? pg0 : pg1) * p.h_kv + hk) * kD + d) * kPage +
+                           (kbase & 63);
+      r.v0 = *reinterpret_cast<const u32x4*>(src);
+      r.v1 = *reinterpret_cast<const u32x4*>(src + 16);
       if (kbase + 32 > kvl) {
-        v0 = zero_tail(v0, kvl - kbase);
-        v1 = zero_tail(v1, kvl - kbase - 16);
+        r.v0 = zero_tail(r.v0, kvl - kbase);
+        r.v1 = zero_tail(r.v1, kvl - kbase - 16);
       }
     }
-    uint8_t* rowp = sm.v + d * kTile;
-    const int sw = v_swz(d);
-    *reinterpret_cast<u32x4*>(rowp + (((2 * part) ^ sw) << 4)) = v0;
-    *reinterpret_cast<u32x4*>(rowp + (((2 * part + 1) ^ sw) << 4)) = v1;
   }
+  r.ds = 0;
   if (t < kTile) {
     const int kabs = j * kTile + t;
-    uint16_t v = 0;
-    if (p.smooth && kabs < kvl) {
-      const int64_t page = pt[kabs >> 6];
-      const float x = bf16_to_f32(p.ds[(page * p.h_q + h) * kPage + (kabs & 63)]) * seed_scale;
-      v = bf16_rne(x);   // exact: a BF16 value times a power of two
-    }
-    sm.ds[t] = v;
+    if (p.smooth && kabs < kvl)
+      r.ds = p.ds[((t < 64 ? pg0 : pg1) * p.h_q + h) * kPage + (kabs & 63)];
   }
 }
 
-template <bool SMOOTH>
+__device__ __forceinline__ void store_tile(PrefillSmem& sm, const TileRegs& r, float seed_scale) {
+  const int t = threadIdx.x;
+  {
+    const int key = t >> 2, qt = t & 3;
+    const ScaleSplit s0 = split_e4m3(r.ksc & 0xFFu), s1 = split_e4m3((r.ksc >> 8) & 0xFFu);
+    uint8_t* rowp = sm.k + key * 256;
+    const int sw = k_swz(key);
+    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 0) ^ sw) << 4)) = dequant8(r.kc[0], s0);
+    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 1) ^ sw) << 4)) = dequant8(r.kc[1], s0);
+    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 2) ^ sw) << 4)) = dequant8(r.kc[2], s1);
+    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 3) ^ sw) << 4)) = dequant8(r.kc[3], s1);
+  }
+  {
+    const int d = t >> 2, part = t & 3;
+    uint8_t* rowp = sm.v + d * kTile;
+    const int sw = v_swz(d);
+    *reinterpret_cast<u32x4*>(rowp + (((2 * part) ^ sw) << 4)) = r.v0;
+    *reinterpret_cast<u32x4*>(rowp + (((2 * part + 1) ^ sw) << 4)) = r.v1;
+  }
+  // exact: a BF16 value times a power of two stays a BF16 value
+  if (t < kTile) sm.ds[t] = bf16_rne(bf16_to_f32((uint16_t)r.ds) * seed_scale);
+}
+
+// How the compensation 1 Delta_S^T (Sec. 4.3 Eq. 11) enters the score
+// accumulator before the QK product:
+//  kSeedMfma  one BF16 rank-one MFMA per 16-key block (A = the block's Delta_S
+//             in reduction slot 0, B = ones in slot 0); it depends on the keys
+//             only, so its result seeds every query block of the wave;
+//  kSeedInit  the same rank-one matrix loaded directly as the accumulator input
+//             of the first FP16 MFMA (bit-identical: both start the accumulator
+//             at the FP32 value of the BF16 Delta_S);
+//  kSeedNone  no compensation (the unsmoothed "direct" variant).
+enum SeedMode { kSeedNone = 0, kSeedMfma = 1, kSeedInit = 2 };
+
+template <int SEED>
 __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
-  __shared__ __attribute__((aligned(16))) PrefillSmem sm;
+  __shared__ __attribute__((aligned(16))) PrefillSmem smem[2];
 
   // ---- work item: largest query tiles first (longest-processing-time order)
   int b, h, rank;
@@ -187,94 +219,109 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     for (int db = 0; db < 8; ++db) o[db][nb] = (f32x4){0.f, 0.f, 0.f, 0.f};
   }
 
+  const int32_t* pt = p.page_table + (int64_t)b * p.max_pages;
+  {
+    TileRegs r0r;
+    fetch_tile(r0r, p, pt, hk, h, j_hi, kvl);
+    store_tile(smem[j_hi & 1], r0r, seed_scale);
+  }
+  __syncthreads();
   for (int j = j_hi; j >= 0; --j) {
-    __syncthreads();
-    load_tile(sm, p, b, hk, h, j, kvl, seed_scale);
-    __syncthreads();
-    if (!wave_active) continue;
+    TileRegs nxt;
+    if (j > 0) fetch_tile(nxt, p, pt, hk, h, j - 1, kvl);
+    const PrefillSmem& sm = smem[j & 1];
     const int key0 = j * kTile;
-    if (key0 > wpos_max) continue;   // tile entirely after every row of this wave
-    const bool need_mask = key0 + kTile - 1 > wpos_min;
-
-    // ---- S^T = seed + K Q^T
-    f32x4 s[8][kNB];
-#pragma unroll
-    for (int mb = 0; mb < 8; ++mb) {
-      const int krow = 32 * (lr >> 2) + 4 * mb + (lr & 3);
-      if (SMOOTH) {
-        bf16x8 aseed = {};
-        if (lane < 16) aseed[0] = __builtin_bit_cast(__bf16, sm.ds[krow]);
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_bf16(aseed, bseed, (f32x4){0.f, 0.f, 0.f, 0.f});
-      } else {
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = (f32x4){0.f, 0.f, 0.f, 0.f};
-      }
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const f16x8 kop = *reinterpret_cast<const f16x8*>(sm.k + krow * 256 + (((4 * ks + g) ^ lr) << 4));
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_f16(kop, qop[nb][ks], s[mb][nb]);
-      }
-    }
-    if (need_mask) {
-#pragma unroll
-      for (int mb = 0; mb < 8; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (key0 + 32 * g + 4 * mb + i > pos[nb]) s[mb][nb][i] = -INFINITY;
-    }
-
-    // ---- online softmax; P (x448) to FP8 in the PV operand layout
-    i32x8 pb[kNB];
-    float alpha[kNB];
-#pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) {
-      float mx = -INFINITY;
-#pragma unroll
-      for (int mb = 0; mb < 8; ++mb)
-        mx = fmaxf(fmaxf(mx, fmaxf(s[mb][nb][0], s[mb][nb][1])), fmaxf(s[mb][nb][2], s[mb][nb][3]));
-      mx = wave_max16(mx);
-      const float mnew = fmaxf(m[nb], mx);
-      const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
-      alpha[nb] = (m[nb] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m[nb] - muse) * lam2);
-      m[nb] = mnew;
-      float ps = 0.0f;
+    if (wave_active && key0 <= wpos_max) {
+      const bool need_mask = key0 + kTile - 1 > wpos_min;
+      f32x4 s[8][kNB];
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) {
-        float e[4];
+        f32x4 seed = (f32x4){0.f, 0.f, 0.f, 0.f};
+        if (SEED == kSeedMfma) {
+          bf16x8 aseed = {};
+          aseed[0] = __builtin_bit_cast(__bf16, lane < 16 ? sm.ds[32 * (lr >> 2) + 4 * mb + (lr & 3)]
+                                                          : (uint16_t)0);
+          seed = mfma_bf16(aseed, bseed, seed);
+        } else if (SEED == kSeedInit) {
+          // keys 32g + 4mb .. +3 of the lane's accumulator rows
+          const uint2 d4 = *reinterpret_cast<const uint2*>(&sm.ds[32 * g + 4 * mb]);
+          seed = (f32x4){__uint_as_float(d4.x << 16), __uint_as_float(d4.x & 0xFFFF0000u),
+                         __uint_as_float(d4.y << 16), __uint_as_float(d4.y & 0xFFFF0000u)};
+        }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][nb][i] - muse, lam2, kLog2_448));
-        ps += (e[0] + e[1]) + (e[2] + e[3]);
-        pb[nb][mb] = (int)pack_fp8x4(e[0], e[1], e[2], e[3]);
+        for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = seed;
       }
-      l[nb] = alpha[nb] * l[nb] + ps;
+#pragma unroll
+      for (int half = 0; half < 2; ++half)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+        for (int mb = 4 * half; mb < 4 * half + 4; ++mb) {
+          const int krow = 32 * (lr >> 2) + 4 * mb + (lr & 3);
+          const f16x8 kop = *reinterpret_cast<const f16x8*>(sm.k + krow * 256 + (((4 * ks + g) ^ lr) << 4));
+#pragma unroll
+          for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_f16(kop, qop[nb][ks], s[mb][nb]);
+        }
+      }
+      if (need_mask) {
+#pragma unroll
+        for (int mb = 0; mb < 8; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < kNB; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (key0 + 32 * g + 4 * mb + i > pos[nb]) s[mb][nb][i] = -INFINITY;
+      }
+      i32x8 pb[kNB];
+      float alpha[kNB];
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int mb = 0; mb < 8; ++mb)
+          mx = fmaxf(fmaxf(mx, fmaxf(s[mb][nb][0], s[mb][nb][1])), fmaxf(s[mb][nb][2], s[mb][nb][3]));
+        mx = wave_max16(mx);
+        const float mnew = fmaxf(m[nb], mx);
+        const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
+        alpha[nb] = (m[nb] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m[nb] - muse) * lam2);
+        m[nb] = mnew;
+        const float bias = __builtin_fmaf(-muse, lam2, kLog2_448);
+        float ps = 0.0f;
+#pragma unroll
+        for (int mb = 0; mb < 8; ++mb) {
+          float e[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][nb][i], lam2, bias));
+          ps += (e[0] + e[1]) + (e[2] + e[3]);
+          pb[nb][mb] = (int)pack_fp8x4(e[0], e[1], e[2], e[3]);
+        }
+        l[nb] = alpha[nb] * l[nb] + ps;
+      }
+      bool moved = false;
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) moved |= alpha[nb] != 1.0f;
+      if (__builtin_amdgcn_ballot_w64(moved) != 0) {
+#pragma unroll
+        for (int db = 0; db < 8; ++db)
+#pragma unroll
+          for (int nb = 0; nb < kNB; ++nb) o[db][nb] *= alpha[nb];
+      }
+#pragma unroll
+      for (int db = 0; db < 8; ++db) {
+        const int d = 16 * db + lr;
+        const uint8_t* vr = sm.v + d * kTile;
+        const int sw = v_swz(d);
+        const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((2 * g) ^ sw) << 4));
+        const u32x4 vb = *reinterpret_cast<const u32x4*>(vr + (((2 * g + 1) ^ sw) << 4));
+        const i32x8 vop = {(int)va[0], (int)va[1], (int)va[2], (int)va[3],
+                           (int)vb[0], (int)vb[1], (int)vb[2], (int)vb[3]};
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb) o[db][nb] = mfma_fp8(vop, pb[nb], o[db][nb]);
+      }
     }
-    bool moved = false;
-#pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) moved |= alpha[nb] != 1.0f;
-    if (__builtin_amdgcn_ballot_w64(moved) != 0) {
-#pragma unroll
-      for (int db = 0; db < 8; ++db)
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) o[db][nb] *= alpha[nb];
-    }
-
-    // ---- O^T += V^T P^T (FP8)
-#pragma unroll
-    for (int db = 0; db < 8; ++db) {
-      const int d = 16 * db + lr;
-      const uint8_t* vr = sm.v + d * kTile;
-      const int sw = v_swz(d);
-      const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((2 * g) ^ sw) << 4));
-      const u32x4 vb = *reinterpret_cast<const u32x4*>(vr + (((2 * g + 1) ^ sw) << 4));
-      const i32x8 vop = {(int)va[0], (int)va[1], (int)va[2], (int)va[3],
-                         (int)vb[0], (int)vb[1], (int)vb[2], (int)vb[3]};
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) o[db][nb] = mfma_fp8(vop, pb[nb], o[db][nb]);
-    }
+    if (j > 0) store_tile(smem[(j - 1) & 1], nxt, seed_scale);
+    __syncthreads();
   }
 
   if (!wave_active) return;
@@ -285,12 +332,13 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     const int row = wrow0 + nb * 16 + lr;
     if (row < nq) {
       uint16_t* dst = p.out + ((int64_t)(q0 + row) * p.h_q + h) * kD;
+      const float inv = __frcp_rn(lt);
 #pragma unroll
       for (int db = 0; db < 8; ++db) {
-        const uint32_t lo = (uint32_t)bf16_rne(__fdiv_rn(o[db][nb][0], lt)) |
-                            ((uint32_t)bf16_rne(__fdiv_rn(o[db][nb][1], lt)) << 16);
-        const uint32_t hi = (uint32_t)bf16_rne(__fdiv_rn(o[db][nb][2], lt)) |
-                            ((uint32_t)bf16_rne(__fdiv_rn(o[db][nb][3], lt)) << 16);
+        const uint32_t lo = (uint32_t)bf16_rne(o[db][nb][0] * inv) |
+                            ((uint32_t)bf16_rne(o[db][nb][1] * inv) << 16);
+        const uint32_t hi = (uint32_t)bf16_rne(o[db][nb][2] * inv) |
+                            ((uint32_t)bf16_rne(o[db][nb][3] * inv) << 16);
         *reinterpret_cast<uint2*>(dst + 16 * db + 4 * g) = make_uint2(lo, hi);
       }
     }
@@ -302,10 +350,12 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream) {
   const unsigned blocks = (unsigned)(p.n_qtiles * p.h_q * p.batch);
   if (blocks == 0) return hipSuccess;
-  if (p.smooth)
-    prefill_kernel<true><<<dim3(blocks), dim3(kThreads), 0, stream>>>(p);
+  if (!p.smooth)
+    prefill_kernel<kSeedNone><<<dim3(blocks), dim3(kThreads), 0, stream>>>(p);
+  else if (p.seed_init)
+    prefill_kernel<kSeedInit><<<dim3(blocks), dim3(kThreads), 0, stream>>>(p);
   else
-    prefill_kernel<false><<<dim3(blocks), dim3(kThreads), 0, stream>>>(p);
+    prefill_kernel<kSeedMfma><<<dim3(blocks), dim3(kThreads), 0, stream>>>(p);
   return hipGetLastError();
 }
 

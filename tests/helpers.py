@@ -94,7 +94,7 @@ class Run:
                 res[k_] = t.detach().cpu().numpy()
         return res
 
-    def prefill_gpu(self, q_start=None, kv_len=None):
+    def prefill_gpu(self, q_start=None, kv_len=None, extra_flags=0):
         mp = self.mp
         B = self.B
         q_start = np.zeros(B, np.int32) if q_start is None else np.asarray(q_start, np.int32)
@@ -103,7 +103,8 @@ class Run:
         T = int(self.cu[-1])
         out = torch.full((T, self.h_q, 128), float("nan"), dtype=torch.bfloat16, device="cuda")
         mp.prefill(self.qq, self.cache, self.stats, self.cu_d, dev(q_start), dev(kv_len),
-                   dev(self.pt), out, max(self.seqlens), mp.SMOOTH if self.smooth else 0)
+                   dev(self.pt), out, max(self.seqlens),
+                   (mp.SMOOTH if self.smooth else 0) | extra_flags)
         torch.cuda.synchronize()
         return bits(out)
 

@@ -102,3 +102,13 @@ def test_prefill_deterministic(orc, mp):
     a = run.prefill_gpu()
     b = run.prefill_gpu()
     assert np.array_equal(a, b)
+
+
+def test_prefill_seed_modes_bit_identical(orc, mp):
+    """The rank-one BF16 MFMA seed and the accumulator-input seed give the same
+    FP32 accumulator start (the BF16 Delta_S value), hence identical outputs."""
+    print("case: seed modes", flush=True)
+    run = H.Run(orc, mp, 29, [700, 45], 8, 2)
+    a = run.prefill_gpu()
+    b = run.prefill_gpu(extra_flags=mp.SEED_INIT)
+    assert np.array_equal(a, b)
