@@ -3,8 +3,10 @@
 //
 // One wave = one (sequence, KV head, partition).  The G = H_q / H_kv query
 // heads of the KV head are packed into the 16-wide MFMA column dimension
-// (GQA packing); the compensation becomes a rank-G seed: A holds the G
-// Delta_S values of each key, B is a G x G identity.  K and V stream straight
+// (GQA packing); the compensation becomes a rank-G term (Delta_S differs per
+// query head), loaded as the input accumulator of the first QK MFMA: each
+// lane's four accumulator rows are four consecutive keys of one query head,
+// one 8-byte load per 16-key block.  K and V stream straight
 // from HBM into registers (no LDS): each lane loads 16 contiguous bytes of
 // NVFP4 codes per key it owns and 32 contiguous FP8 bytes of the channel-major
 // V page, dequantizes K exactly to FP16 and runs the same S^T = K Q^T /
@@ -19,93 +21,167 @@ namespace mpfa {
 namespace {
 
 constexpr int kWavesPerBlock = 4;
+constexpr int kVBytes = kD * kTile;   // one FP8 V tile per wave in LDS (16 KB)
 
-__global__ __launch_bounds__(kWavesPerBlock * 64) void decode_kernel(DecodeParams p) {
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) void* global_ptr_t;
+
+// Software pipeline per wave, iteration j (tiles last to first):
+//   wait for every outstanding load;  PV of tile j+1 (V from LDS, P from
+//   registers);  direct global->LDS loads of V tile j;  QK of tile j (K codes
+//   prefetched in registers);  prefetch of tile j-1's K codes, scales and
+//   compensation;  online softmax of tile j.
+// V never occupies registers (it is read from LDS as MFMA operands), which
+// keeps the wave under the register budget of two waves per SIMD.
+// LDS V layout: for channel block db and half hf, the 1 KB slab at
+// (2 db + hf) KB holds, at 16 * lane, the bytes the lane feeds to the MFMA:
+// channel 16 db + lane%16, keys 32 (lane/16) + 16 hf .. +15.
+template <bool SMOOTH>
+__global__ __launch_bounds__(kWavesPerBlock * 64, 2) void decode_kernel(DecodeParams p) {
+  __shared__ __attribute__((aligned(16))) uint8_t vlds[kWavesPerBlock * kVBytes];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 4, lr = lane & 15;
   const int part = blockIdx.x * kWavesPerBlock + wave;
   const int hk = blockIdx.y, b = blockIdx.z;
   const int kvl = p.kv_len[b];
   const int np = (kvl + p.partition_tokens - 1) / p.partition_tokens;
   if (part >= np) return;
+  uint8_t* vbuf = vlds + wave * kVBytes;
   const int grp = p.h_q / p.h_kv;
   const int kbeg = part * p.partition_tokens;
   const int kend = min(kbeg + p.partition_tokens, kvl);
   const bool qvalid = lr < grp;
   const int h = hk * grp + (qvalid ? lr : 0);
   const int32_t* pt = p.page_table + (int64_t)b * p.max_pages;
+  const int npg = (kvl + 63) >> 6;
 
-  const float tk = p.k_tscale[b * p.h_kv + hk];
-  const int ek = ilog2f(tk);
-  const float tq = p.q_tscale[b * p.h_q + h];
-  const int eqk = ilog2f(tq) + ek;
-  const float lam2 = __builtin_ldexpf(p.lam, eqk);   // per query head (column lr)
+  const int ek = ilog2f(p.k_tscale[b * p.h_kv + hk]);
+  const int eqk = ilog2f(p.q_tscale[b * p.h_q + h]) + ek;
+  const float lam2 = __builtin_ldexpf(p.lam, eqk);           // per query head (column lr)
+  const float seed_scale = __builtin_ldexpf(1.0f, -eqk);     // Delta_S in accumulator units
 
   // Q operand: column lr = query head hk*G + lr; channels 32g + 8ks + e
   f16x8 qop[4];
   {
     const uint8_t* qc = p.q_codes + ((int64_t)b * p.h_q + h) * 64;
     const uint8_t* qsc = p.q_scales + ((int64_t)b * p.h_q + h) * 8;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const uint32_t cw = qvalid ? *reinterpret_cast<const uint32_t*>(qc + 16 * g + 4 * ks) : 0u;
-      const uint32_t sc = qvalid ? qsc[2 * g + (ks >> 1)] : 0u;
-      qop[ks] = dequant8(cw, split_e4m3(sc));
-    }
+    const u32x4 cw = qvalid ? *reinterpret_cast<const u32x4*>(qc + 16 * g) : (u32x4){0u, 0u, 0u, 0u};
+    const uint32_t sc = qvalid ? *reinterpret_cast<const uint16_t*>(qsc + 2 * g) : 0u;
+    const ScaleSplit s0 = split_e4m3(sc & 0xFFu), s1 = split_e4m3((sc >> 8) & 0xFFu);
+    qop[0] = dequant8(cw[0], s0);
+    qop[1] = dequant8(cw[1], s0);
+    qop[2] = dequant8(cw[2], s1);
+    qop[3] = dequant8(cw[3], s1);
   }
-  // seed operands: lanes 0..15 carry reduction index e = query head slot
-  bf16x8 bseed = {};
-  if (lane < 16 && lane < grp) bseed[lane & 7] = (__bf16)1.0f;
-  float seed_scale[8];
+
+  const int krow_in_tile = 32 * (lr >> 2) + (lr & 3);   // + 4 mb: key of MFMA row lr
+  const int64_t page_k_rows = (int64_t)p.h_kv * kPage;   // K rows per page
+  const int64_t kv_head = (int64_t)hk * kPage;
+
+  // ---- K-side loads of one tile (registers).  Every address stays inside a
+  // mapped page (page index clamped to the sequence's last page), so the loads
+  // are unconditional; keys at or past the partition end are masked to -inf
+  // after QK, which also discards whatever those cache slots hold.
+  u32x4 kc[8];
+  uint32_t ksc[8];
+  uint2 dsw[8];
+  auto load_k = [&](int j) {
+    const int64_t pg0 = pt[min(2 * j, npg - 1)];
+    const int64_t pg1 = pt[min(2 * j + 1, npg - 1)];
+    const int64_t kpage = (lr < 8) ? pg0 : pg1;     // MFMA rows 0..7 hold keys 0..63
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    seed_scale[e] = 0.0f;
-    if (e < grp) {
-      const float tqe = p.q_tscale[b * p.h_q + hk * grp + e];
-      seed_scale[e] = __builtin_ldexpf(1.0f, -(ilog2f(tqe) + ek));
+    for (int mb = 0; mb < 8; ++mb) {
+      const int64_t row = kpage * page_k_rows + kv_head + ((krow_in_tile + 4 * mb) & 63);
+      kc[mb] = *reinterpret_cast<const u32x4*>(p.k_codes + row * 64 + 16 * g);
+      ksc[mb] = *reinterpret_cast<const uint16_t*>(p.k_scales + row * 8 + 2 * g);
     }
-  }
+    // compensation of the lane's accumulator rows: keys 32g + 4mb .. +3, head lr
+    if (SMOOTH) {
+      const int64_t dpage = (g < 2) ? pg0 : pg1;
+      const uint16_t* dsp = p.ds + (dpage * p.h_q + h) * kPage + ((32 * g) & 63);
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) dsw[mb] = *reinterpret_cast<const uint2*>(dsp + 4 * mb);
+    } else {
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) dsw[mb] = make_uint2(0u, 0u);
+    }
+  };
+  // ---- V tile j: 16 direct global->LDS loads of 16 bytes per lane
+  auto load_v = [&](int j) {
+    const int64_t vpage = pt[min(2 * j + (g >> 1), npg - 1)];
+    const uint8_t* vsrc = p.v_codes + ((vpage * p.h_kv + hk) * kD + lr) * kPage + ((32 * g) & 63);
+#pragma unroll
+    for (int db = 0; db < 8; ++db)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+        __builtin_amdgcn_global_load_lds((global_ptr_t)(vsrc + db * 16 * kPage + 16 * hf),
+                                         (lds_ptr_t)(vbuf + (2 * db + hf) * 1024), 16, 0, 0);
+  };
 
   float m = -INFINITY, l = 0.0f;
   f32x4 o[8];
 #pragma unroll
   for (int db = 0; db < 8; ++db) o[db] = (f32x4){0.f, 0.f, 0.f, 0.f};
+  i32x8 pb = {};
+  int pv_tile = -1;      // tile whose P (pb) awaits its PV product
+
+  // O^T += V^T P^T for tile pv_tile.  Keys past the end of the sequence carry
+  // P = 0, but their V bytes may be stale cache contents: they are cleared so
+  // that 0 * NaN cannot occur.
+  auto pv = [&]() {
+    u32x4 va[8], vb[8];
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      va[db] = *reinterpret_cast<const u32x4*>(vbuf + (2 * db) * 1024 + 16 * lane);
+      vb[db] = *reinterpret_cast<const u32x4*>(vbuf + (2 * db + 1) * 1024 + 16 * lane);
+    }
+    if (pv_tile * kTile + kTile > kend) {   // uniform: the partition's last keys
+      const int nv = kend - (pv_tile * kTile + 32 * g);
+      uint32_t ma[4], mb2[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int k1 = nv - 4 * i, k2 = nv - 16 - 4 * i;
+        ma[i] = k1 >= 4 ? 0xFFFFFFFFu : (k1 <= 0 ? 0u : ((1u << (8 * k1)) - 1u));
+        mb2[i] = k2 >= 4 ? 0xFFFFFFFFu : (k2 <= 0 ? 0u : ((1u << (8 * k2)) - 1u));
+      }
+#pragma unroll
+      for (int db = 0; db < 8; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          va[db][i] &= ma[i];
+          vb[db][i] &= mb2[i];
+        }
+    }
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      const i32x8 vop = {(int)va[db][0], (int)va[db][1], (int)va[db][2], (int)va[db][3],
+                         (int)vb[db][0], (int)vb[db][1], (int)vb[db][2], (int)vb[db][3]};
+      o[db] = mfma_fp8(vop, pb, o[db]);
+    }
+  };
 
   const int j_lo = kbeg / kTile, j_hi = (kend - 1) / kTile;
+  load_k(j_hi);
   for (int j = j_hi; j >= j_lo; --j) {
     const int key0 = j * kTile;
+    __builtin_amdgcn_s_waitcnt(0);   // K(j) in registers, V(j+1) in LDS
+    if (pv_tile >= 0) pv();
+    // the LDS reads of PV(j+1) must be complete before V(j) overwrites them
+    __builtin_amdgcn_s_waitcnt(0);
+    load_v(j);
+    // ---- S^T = 1 Delta_S^T + K Q^T (the rank-G term as accumulator input)
     f32x4 s[8];
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb) {
-      const int kabs = key0 + 32 * (lr >> 2) + 4 * mb + (lr & 3);
-      u32x4 codes = {0u, 0u, 0u, 0u};
-      uint32_t sc = 0;
-      int64_t page = 0;
-      const bool kin = kabs < kend;
-      if (kin) {
-        page = pt[kabs >> 6];
-        const int64_t row = (page * p.h_kv + hk) * kPage + (kabs & 63);
-        codes = *reinterpret_cast<const u32x4*>(p.k_codes + row * 64 + 16 * g);
-        sc = *reinterpret_cast<const uint16_t*>(p.k_scales + row * 8 + 2 * g);
-      }
-      if (p.smooth) {
-        bf16x8 aseed = {};
-        if (lane < 16 && kin) {
-          const uint16_t* dsp = p.ds + (page * p.h_q + hk * grp) * kPage + (kabs & 63);
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (e < grp)
-              aseed[e] = __builtin_bit_cast(__bf16, bf16_rne(bf16_to_f32(dsp[e * kPage]) * seed_scale[e]));
-        }
-        s[mb] = mfma_bf16(aseed, bseed, (f32x4){0.f, 0.f, 0.f, 0.f});
-      } else {
-        s[mb] = (f32x4){0.f, 0.f, 0.f, 0.f};
-      }
-      const ScaleSplit s0 = split_e4m3(sc & 0xFFu), s1 = split_e4m3((sc >> 8) & 0xFFu);
-      s[mb] = mfma_f16(dequant8(codes[0], s0), qop[0], s[mb]);
-      s[mb] = mfma_f16(dequant8(codes[1], s0), qop[1], s[mb]);
-      s[mb] = mfma_f16(dequant8(codes[2], s1), qop[2], s[mb]);
-      s[mb] = mfma_f16(dequant8(codes[3], s1), qop[3], s[mb]);
+      f32x4 c = (f32x4){__uint_as_float(dsw[mb].x << 16), __uint_as_float(dsw[mb].x & 0xFFFF0000u),
+                        __uint_as_float(dsw[mb].y << 16), __uint_as_float(dsw[mb].y & 0xFFFF0000u)};
+      c *= seed_scale;   // exact: power of two
+      const ScaleSplit s0 = split_e4m3(ksc[mb] & 0xFFu), s1 = split_e4m3((ksc[mb] >> 8) & 0xFFu);
+      c = mfma_f16(dequant8(kc[mb][0], s0), qop[0], c);
+      c = mfma_f16(dequant8(kc[mb][1], s0), qop[1], c);
+      c = mfma_f16(dequant8(kc[mb][2], s1), qop[2], c);
+      s[mb] = mfma_f16(dequant8(kc[mb][3], s1), qop[3], c);
     }
+    if (j > j_lo) load_k(j - 1);
     if (key0 + kTile > kend) {
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb)
@@ -113,6 +189,7 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_kernel(DecodeParam
         for (int i = 0; i < 4; ++i)
           if (key0 + 32 * g + 4 * mb + i >= kend) s[mb][i] = -INFINITY;
     }
+    // ---- online softmax (rows = query heads), P to FP8 (x448)
     float mx = -INFINITY;
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb)
@@ -122,13 +199,13 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_kernel(DecodeParam
     const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
     const float alpha = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m - muse) * lam2);
     m = mnew;
-    i32x8 pb;
+    const float bias = __builtin_fmaf(-muse, lam2, kLog2_448);
     float ps = 0.0f;
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb) {
       float e[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i] - muse, lam2, kLog2_448));
+      for (int i = 0; i < 4; ++i) e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][i], lam2, bias));
       ps += (e[0] + e[1]) + (e[2] + e[3]);
       pb[mb] = (int)pack_fp8x4(e[0], e[1], e[2], e[3]);
     }
@@ -137,32 +214,16 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_kernel(DecodeParam
 #pragma unroll
       for (int db = 0; db < 8; ++db) o[db] *= alpha;
     }
-    // V^T operand: channel d = 16 db + lr, keys 32g .. 32g+31 of the tile
-    const int kv0 = key0 + 32 * g;
-    const bool vin = kv0 < kend;
-    int64_t vpage = vin ? pt[kv0 >> 6] : 0;
-#pragma unroll
-    for (int db = 0; db < 8; ++db) {
-      u32x4 va = {0u, 0u, 0u, 0u}, vb = {0u, 0u, 0u, 0u};
-      if (vin) {
-        const uint8_t* src = p.v_codes + ((vpage * p.h_kv + hk) * kD + 16 * db + lr) * kPage + (kv0 & 63);
-        va = *reinterpret_cast<const u32x4*>(src);
-        vb = *reinterpret_cast<const u32x4*>(src + 16);
-        if (kv0 + 32 > kend) {
-          const int nv = kend - kv0;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            int k1 = nv - 4 * i, k2 = nv - 16 - 4 * i;
-            va[i] &= k1 >= 4 ? 0xFFFFFFFFu : (k1 <= 0 ? 0u : ((1u << (8 * k1)) - 1u));
-            vb[i] &= k2 >= 4 ? 0xFFFFFFFFu : (k2 <= 0 ? 0u : ((1u << (8 * k2)) - 1u));
-          }
-        }
-      }
-      const i32x8 vop = {(int)va[0], (int)va[1], (int)va[2], (int)va[3],
-                         (int)vb[0], (int)vb[1], (int)vb[2], (int)vb[3]};
-      o[db] = mfma_fp8(vop, pb, o[db]);
-    }
+    pv_tile = j;
   }
+  __builtin_amdgcn_s_waitcnt(0);
+  pv();
+  // The scaled FP8 MFMA may otherwise be sunk into the branch below, where
+  // lanes of the invalid query-head columns are switched off; the MFMA then
+  // reads their (inactive) operand rows as zero.  An empty asm that consumes
+  // the accumulators keeps the products in full-wave control flow.
+#pragma unroll
+  for (int db = 0; db < 8; ++db) asm volatile("" : "+v"(o[db]));
 
   // partition state: m in log2 units (m * lambda'), l, O[128]
   const float lt = wave_sum16(l);
@@ -202,7 +263,10 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeParams p) {
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
   if (p.batch == 0) return hipSuccess;
   const dim3 grid((p.max_partitions + kWavesPerBlock - 1) / kWavesPerBlock, p.h_kv, p.batch);
-  decode_kernel<<<grid, dim3(kWavesPerBlock * 64), 0, stream>>>(p);
+  if (p.smooth)
+    decode_kernel<true><<<grid, dim3(kWavesPerBlock * 64), 0, stream>>>(p);
+  else
+    decode_kernel<false><<<grid, dim3(kWavesPerBlock * 64), 0, stream>>>(p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   merge_kernel<<<dim3(p.h_q, p.batch), dim3(128), 0, stream>>>(p);
