@@ -28,6 +28,46 @@ PEAK_FP8 = 5.0e15         # dense FP8
 PEAK_BF16 = 2.5e15        # dense BF16 / FP16
 PEAK_HBM = 8.0e12         # bytes/s
 
+# HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE passes,
+# scaled by what the same counters read for a plain device copy.  A figure is
+# reported only while the kernel's sources hash to the value recorded with it.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.txt")
+KERNEL_SOURCES = {
+    "prefill_kernel": ["csrc/prefill.hip", "csrc/mpfa_device.h", "csrc/mpfa_internal.h", "csrc/api.cpp"],
+    "decode_kernel": ["csrc/decode.hip", "csrc/mpfa_device.h", "csrc/mpfa_internal.h", "csrc/api.cpp"],
+}
+
+
+def source_hash(kernel: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2609_33135_amd", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or None
+    when there is none or the kernel's sources changed since it was taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    with open(TRAFFIC_FILE) as fh:
+        for line in fh:
+            line = line.split("#", 1)[0].strip()
+            if "=" in line:
+                k, v = (x.strip() for x in line.split("=", 1))
+                kv[k] = v
+    try:
+        if kv[f"{kernel}.source_sha256"] != source_hash(kernel):
+            return None
+        kib = 1024.0
+        return (float(kv[f"{kernel}.fetch_kib"]) * float(kv["fetch_factor"])
+                + float(kv[f"{kernel}.write_kib"]) * float(kv["write_factor"])) * kib
+    except KeyError:
+        return None
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -222,8 +262,9 @@ def main():
         res["prefill"] = {"ms": prefill_ms, "tflops": achieved / 1e12, "quant_ms": quant_ms,
                           "causal_pairs": pairs, "flop": flops}
         res["roofline"] = {"bound": "mfma", "achieved": achieved / 1e12, "peak": peak / 1e12,
-                           "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
-                           "kernel": "prefill_kernel<true>",
+                           "unit": "TFLOP/s", "frac": achieved / peak,
+                           "traffic": measured_traffic("prefill_kernel"),
+                           "kernel": "prefill_kernel<kSeedMfma>",
                            "peak_note": "time-weighted FP4 (QK) + FP8 (PV) dense peak; exact-NVFP4 "
                                         "path peak (FP16 QK + FP8 PV) is "
                                         f"{flops / (f_qk / PEAK_BF16 + f_pv / PEAK_FP8) / 1e12:.0f}"}
@@ -278,7 +319,8 @@ def main():
         nbytes = decode_bytes(sd)
         gbs = nbytes / (decode_ms * 1e-3) / 1e9
         res["decode"] = {"ms": decode_ms, "GB/s": gbs, "frac_hbm": gbs * 1e9 / PEAK_HBM,
-                         "bytes": nbytes, "partition_tokens": sd["part"],
+                         "bytes": nbytes, "traffic": measured_traffic("decode_kernel"),
+                         "partition_tokens": sd["part"],
                          "keys": int(sum(sd["lens"]))}
 
     if args.copy_calibration:
