@@ -10,73 +10,110 @@
 
 namespace mpfa {
 
-// One workgroup per (sequence, head).  1024 threads = 8 token blocks in flight
-// x 128 channels.  Means: FP32 sum inside each 128-token block in token order,
-// then the block partials in block order (thread group 0 adds them), FP32
-// division, BF16 rounding.  Then the amax of the centered values gives the
-// power-of-two tensor scale.
+// One workgroup per (sequence, head), 16 waves.  Each wave sums one 128-token
+// block at a time (lane l owns channels 2l, 2l+1; loads issued 16 tokens
+// ahead), FP32 in token order; wave 0 then adds the block partials in block
+// order, divides in FP32 and rounds to BF16.  A second pass takes the amax of
+// the centered values for the power-of-two tensor scale.
 __global__ __launch_bounds__(1024) void stats_kernel(QuantParams p) {
-  __shared__ float part[8][kD];
+  constexpr int kW = 16;                     // waves per workgroup
+  __shared__ float part[kW][kD];
   __shared__ float meanf[kD];
-  __shared__ float red[32];
+  __shared__ float red[kW];
   const int Htot = p.stats_k ? p.h_q + p.h_kv : p.h_q;
   const int b = blockIdx.x / Htot;
   const int hh = blockIdx.x % Htot;
   const bool is_k = hh >= p.h_q;
   const int h = is_k ? hh - p.h_q : hh;
   const int H = is_k ? p.h_kv : p.h_q;
-  const uint16_t* x = is_k ? p.k : p.q;
-  const int c = threadIdx.x & 127, slot = threadIdx.x >> 7;
+  const uint32_t* x = reinterpret_cast<const uint32_t*>(is_k ? p.k : p.q);   // BF16 pairs
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int c0 = 2 * lane;
   const int64_t t0 = p.cu_seqlens[b];
   const int n = p.cu_seqlens[b + 1] - p.cu_seqlens[b];
   uint16_t* mean_out = (is_k ? p.k_mean : p.q_mean) + ((int64_t)b * H + h) * kD;
+  // BF16 pair of token t (relative to the sequence) for this lane's channels
+  auto row = [&](int t) { return x[((t0 + t) * H + h) * (kD / 2) + lane]; };
 
   if (p.compute_stats) {
-    float total = 0.0f;
+    float tot0 = 0.0f, tot1 = 0.0f;
     if (p.smooth && n > 0) {
       const int nblk = (n + 127) / 128;
-      for (int blk0 = 0; blk0 < nblk; blk0 += 8) {
-        const int blk = blk0 + slot;
-        float s = 0.0f;
+      for (int blk0 = 0; blk0 < nblk; blk0 += kW) {
+        const int blk = blk0 + wv;
+        float s0 = 0.0f, s1 = 0.0f;
         if (blk < nblk) {
-          const int e = min(n, blk * 128 + 128);
-          for (int t = blk * 128; t < e; ++t)
-            s += bf16_to_f32(x[((t0 + t) * H + h) * kD + c]);
+          const int tb = blk * 128, te = min(n, tb + 128);
+          for (int t = tb; t < te; t += 16) {
+            uint32_t v[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) v[u] = (t + u < te) ? row(t + u) : 0u;
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+              if (t + u < te) {
+                s0 += __uint_as_float(v[u] << 16);
+                s1 += __uint_as_float(v[u] & 0xFFFF0000u);
+              }
+            }
+          }
         }
-        part[slot][c] = s;
+        part[wv][c0] = s0;
+        part[wv][c0 + 1] = s1;
         __syncthreads();
-        if (slot == 0)
-          for (int j = 0; j < 8 && blk0 + j < nblk; ++j) total += part[j][c];
+        if (wv == 0) {
+          for (int j = 0; j < kW && blk0 + j < nblk; ++j) {
+            tot0 += part[j][c0];
+            tot1 += part[j][c0 + 1];
+          }
+        }
         __syncthreads();
       }
     }
-    if (slot == 0) {
-      uint16_t mb = 0;
-      if (p.smooth && n > 0) mb = bf16_rne(__fdiv_rn(total, (float)n));
-      mean_out[c] = mb;
-      meanf[c] = bf16_to_f32(mb);
+    if (wv == 0) {
+      uint16_t m0 = 0, m1 = 0;
+      if (p.smooth && n > 0) {
+        m0 = bf16_rne(__fdiv_rn(tot0, (float)n));
+        m1 = bf16_rne(__fdiv_rn(tot1, (float)n));
+      }
+      mean_out[c0] = m0;
+      mean_out[c0 + 1] = m1;
+      meanf[c0] = bf16_to_f32(m0);
+      meanf[c0 + 1] = bf16_to_f32(m1);
     }
-  } else if (slot == 0) {
-    meanf[c] = p.smooth ? bf16_to_f32(mean_out[c]) : 0.0f;
+  } else if (wv == 0) {
+    meanf[c0] = p.smooth ? bf16_to_f32(mean_out[c0]) : 0.0f;
+    meanf[c0 + 1] = p.smooth ? bf16_to_f32(mean_out[c0 + 1]) : 0.0f;
   }
   __syncthreads();
 
-  // amax of the centered values
+  // amax of the centered values (any order)
   float amax = 0.0f;
-  const float mc = meanf[c];
-  for (int t = slot; t < n; t += 8) {
-    float xc = bf16_to_f32(x[((t0 + t) * H + h) * kD + c]) - mc;
-    amax = fmaxf(amax, __builtin_fabsf(xc));
+  const float m0 = meanf[c0], m1 = meanf[c0 + 1];
+  int t = wv;
+  for (; t + 3 * kW < n; t += 4 * kW) {
+    uint32_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = row(t + u * kW);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      amax = fmaxf(amax, __builtin_fabsf(__uint_as_float(v[u] << 16) - m0));
+      amax = fmaxf(amax, __builtin_fabsf(__uint_as_float(v[u] & 0xFFFF0000u) - m1));
+    }
+  }
+  for (; t < n; t += kW) {
+    const uint32_t v = row(t);
+    amax = fmaxf(amax, __builtin_fabsf(__uint_as_float(v << 16) - m0));
+    amax = fmaxf(amax, __builtin_fabsf(__uint_as_float(v & 0xFFFF0000u) - m1));
   }
   for (int off = 32; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = amax;
+  if (lane == 0) red[wv] = amax;
   __syncthreads();
   if (threadIdx.x == 0) {
     float a = 0.0f;
-    for (int i = 0; i < 16; ++i) a = fmaxf(a, red[i]);
-    float t = p.tscale_unit ? 1.0f : tensor_scale(a);
-    if (is_k) p.k_tscale[b * p.h_kv + h] = t;
-    else p.q_tscale[b * p.h_q + h] = t;
+    for (int i = 0; i < kW; ++i) a = fmaxf(a, red[i]);
+    const float ts = p.tscale_unit ? 1.0f : tensor_scale(a);
+    if (is_k) p.k_tscale[b * p.h_kv + h] = ts;
+    else p.q_tscale[b * p.h_q + h] = ts;
   }
 }
 

@@ -112,3 +112,24 @@ def test_prefill_seed_modes_bit_identical(orc, mp):
     a = run.prefill_gpu()
     b = run.prefill_gpu(extra_flags=mp.SEED_INIT)
     assert np.array_equal(a, b)
+
+
+def test_prefill_repeatable_all_modes(orc, mp):
+    """Every seed mode gives bit-identical outputs over repeated launches (a
+    missing synchronisation or an unsatisfied hardware hazard shows up as
+    run-to-run differences), and the two placements of the compensation agree."""
+    print("case: repeatability", flush=True)
+    run = H.Run(orc, mp, 17, [1, 130, 300, 513], 8, 2, outliers=True, smooth=True)
+    first = {}
+    for _ in range(12):
+        for fl in (0, mp.SEED_INIT):
+            out = run.prefill_gpu(extra_flags=fl)
+            if fl in first:
+                assert np.array_equal(out, first[fl]), f"flags {fl}: output changed between launches"
+            else:
+                first[fl] = out
+    assert np.array_equal(first[0], first[mp.SEED_INIT])
+    direct = H.Run(orc, mp, 17, [1, 130, 300, 513], 8, 2, outliers=True, smooth=False)
+    a = direct.prefill_gpu()
+    for _ in range(6):
+        assert np.array_equal(direct.prefill_gpu(), a)
