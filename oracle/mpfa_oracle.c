@@ -267,6 +267,43 @@ void orc_nvfp4_dequant_row(const uint8_t* codes64, const uint8_t* scales8, doubl
     }
 }
 
+void orc_mxfp4_row(const float* xc, uint8_t* codes64, uint8_t* scales8)
+{
+    uint8_t code[ORC_D];
+    for (int g = 0; g < 4; ++g) {
+        double a = 0.0;
+        for (int i = 0; i < 32; ++i) {
+            double ax = fabs((double)xc[g * 32 + i]);
+            if (ax > a) a = ax;
+        }
+        int e = -127;
+        if (a > 0.0) {
+            int ex;
+            frexp(a, &ex);                 /* a = m * 2^ex, m in [0.5, 1) */
+            e = (ex - 1) - 2;              /* floor(log2 a) - 2 */
+            if (e < -127) e = -127;
+            if (e > 127) e = 127;
+        }
+        scales8[g] = (uint8_t)(e + 127);
+        for (int i = 0; i < 32; ++i) {
+            double y = ldexp((double)xc[g * 32 + i], -e);    /* exact */
+            code[g * 32 + i] = orc_e2m1_encode(y);
+        }
+    }
+    for (int g = 4; g < 8; ++g) scales8[g] = 0;
+    for (int j = 0; j < ORC_D / 2; ++j)
+        codes64[j] = (uint8_t)(code[2 * j] | (code[2 * j + 1] << 4));
+}
+
+void orc_mxfp4_dequant_row(const uint8_t* codes64, const uint8_t* scales8, double* out)
+{
+    for (int c = 0; c < ORC_D; ++c) {
+        uint8_t byte = codes64[c / 2];
+        uint8_t code = (c & 1) ? (byte >> 4) : (byte & 15);
+        out[c] = ldexp(orc_e2m1_value(code), (int)scales8[c / 32] - 127);
+    }
+}
+
 /* Algorithm 1 stage one, fused with the cache write (Sec. 5.1, Sec. 6):
  * statistics (first prefill only, then frozen), centering, NVFP4 Q and K,
  * FP8 V (no scale, not centered, Sec. 4.2), and Delta_S = Qbar . K_c per key
@@ -279,7 +316,8 @@ int orc_quantize_qk(const orc_quant_args* a)
     if (B < 0 || Hq <= 0 || Hkv <= 0 || Hkv > 64 || Hq % Hkv) return -1;
     const int smooth = (a->flags & ORC_SMOOTH) != 0;
     const int stats = (a->flags & ORC_COMPUTE_STATS) != 0;
-    const int tunit = (a->flags & ORC_TSCALE_UNIT) != 0;
+    const int mx = (a->flags & ORC_MXFP4) != 0;
+    const int tunit = (a->flags & ORC_TSCALE_UNIT) != 0 || mx;   /* MXFP4: no tensor scale */
     const int grp = Hq / Hkv;
 
     for (int b = 0; b < B; ++b) {
@@ -318,8 +356,11 @@ int orc_quantize_qk(const orc_quant_args* a)
                 const uint16_t* mean = a->q_mean + ((int64_t)b * Hq + h) * ORC_D;
                 for (int c = 0; c < ORC_D; ++c)
                     xc[c] = orc_bf16_value(x[c]) - (smooth ? orc_bf16_value(mean[c]) : 0.0f);
-                orc_nvfp4_row(xc, a->q_tscale[(int64_t)b * Hq + h],
-                              a->q_codes + (tok * Hq + h) * 64, a->q_scales + (tok * Hq + h) * 8);
+                if (mx)
+                    orc_mxfp4_row(xc, a->q_codes + (tok * Hq + h) * 64, a->q_scales + (tok * Hq + h) * 8);
+                else
+                    orc_nvfp4_row(xc, a->q_tscale[(int64_t)b * Hq + h],
+                                  a->q_codes + (tok * Hq + h) * 64, a->q_scales + (tok * Hq + h) * 8);
             }
             for (int h = 0; h < Hkv; ++h) {
                 const uint16_t* x = a->k + (tok * Hkv + h) * ORC_D;
@@ -328,8 +369,11 @@ int orc_quantize_qk(const orc_quant_args* a)
                 for (int c = 0; c < ORC_D; ++c)
                     kch[c] = orc_bf16_value(x[c]) - (smooth ? orc_bf16_value(mean[c]) : 0.0f);
                 int64_t row = (page * Hkv + h) * ORC_PAGE + off;
-                orc_nvfp4_row(kch, a->k_tscale[(int64_t)b * Hkv + h],
-                              a->k_codes + row * 64, a->k_scales + row * 8);
+                if (mx)
+                    orc_mxfp4_row(kch, a->k_codes + row * 64, a->k_scales + row * 8);
+                else
+                    orc_nvfp4_row(kch, a->k_tscale[(int64_t)b * Hkv + h],
+                                  a->k_codes + row * 64, a->k_scales + row * 8);
                 const uint16_t* vx = a->v + (tok * Hkv + h) * ORC_D;
                 for (int c = 0; c < ORC_D; ++c)
                     a->v_codes[((page * Hkv + h) * ORC_D + c) * ORC_PAGE + off] =
@@ -505,7 +549,10 @@ static void gather_kv(const orc_cache* c, int b, int hk, int64_t n, double* kd, 
         int64_t page = c->page_table[(int64_t)b * c->max_pages + key / ORC_PAGE];
         int64_t off = key % ORC_PAGE;
         int64_t row = (page * c->h_kv + hk) * ORC_PAGE + off;
-        orc_nvfp4_dequant_row(c->k_codes + row * 64, c->k_scales + row * 8, tk, kd + key * ORC_D);
+        if (c->flags & ORC_MXFP4)
+            orc_mxfp4_dequant_row(c->k_codes + row * 64, c->k_scales + row * 8, kd + key * ORC_D);
+        else
+            orc_nvfp4_dequant_row(c->k_codes + row * 64, c->k_scales + row * 8, tk, kd + key * ORC_D);
         for (int d = 0; d < ORC_D; ++d)
             vd[key * ORC_D + d] =
                 orc_e4m3_value(c->v_codes[((page * c->h_kv + hk) * ORC_D + d) * ORC_PAGE + off]);
@@ -573,9 +620,13 @@ static int run_items(const orc_cache* c, const int32_t* cu_seqlens, const int32_
                 pos = (int64_t)q_start[b] + item_row[it];
             }
             double qd[ORC_D];
-            orc_nvfp4_dequant_row(c->q_codes + (qtok * c->h_q + h) * 64,
-                                  c->q_scales + (qtok * c->h_q + h) * 8,
-                                  (double)c->q_tscale[(int64_t)b * c->h_q + h], qd);
+            if (c->flags & ORC_MXFP4)
+                orc_mxfp4_dequant_row(c->q_codes + (qtok * c->h_q + h) * 64,
+                                      c->q_scales + (qtok * c->h_q + h) * 8, qd);
+            else
+                orc_nvfp4_dequant_row(c->q_codes + (qtok * c->h_q + h) * 64,
+                                      c->q_scales + (qtok * c->h_q + h) * 8,
+                                      (double)c->q_tscale[(int64_t)b * c->h_q + h], qd);
             const double* dsh = smooth ? dsd + (int64_t)(h - hk * grp) * n : NULL;
             int64_t part = decode_part > 0 ? decode_part : (n > 0 ? n : 1);
             int64_t nparts = n > 0 ? (n + part - 1) / part : 1;

@@ -44,6 +44,8 @@ extern "C" {
 #define ORC_SMOOTH        1   /* sequence centering + Delta_S compensation   */
 #define ORC_COMPUTE_STATS 2   /* compute means / tensor scales (first prefill) */
 #define ORC_TSCALE_UNIT   4   /* tensor scale fixed to 1 (Eq. 1 literally)   */
+#define ORC_MXFP4         8   /* Q/K as MXFP4: E8M0 scale per 32, tensor scale 1
+                                 (also set in orc_cache.flags for the attention) */
 
 #define ORC_QUANT_P       1   /* attention core: round 448*P to E4M3         */
 #define ORC_REVERSE       2   /* attention core: visit KV tiles last to first */
@@ -138,7 +140,7 @@ void orc_attention_textbook(const double* q, const double* k, const double* v,
 
 /* ---- product-shaped attention over the quantized paged cache -------------- */
 typedef struct {
-    int32_t batch, h_q, h_kv, max_pages, flags;  /* flags: ORC_SMOOTH      */
+    int32_t batch, h_q, h_kv, max_pages, flags;  /* flags: ORC_SMOOTH, ORC_MXFP4 */
     const int32_t*  page_table;   /* [batch][max_pages]                    */
     const int32_t*  kv_len;       /* [batch]                               */
     const uint8_t*  k_codes;      /* [pages][h_kv][64][64]                 */
@@ -165,6 +167,15 @@ int orc_prefill(const orc_cache* c, const int32_t* cu_seqlens, const int32_t* q_
 int orc_decode(const orc_cache* c, int32_t partition_tokens,
                int64_t n_items, const int32_t* item_b, const int32_t* item_h,
                uint16_t* out_bf16, double* out_f64);
+
+/* MXFP4 row (the 32-element E8M0 variant Eq. 1 names as the MX format):
+ * per 32-channel block, X = 2^e with e = floor(log2 amax) - 2 (the largest
+ * E2M1 exponent is 2), clamped to [-127, 127] (e = -127 when amax = 0);
+ * code = E2M1(x / X), round to nearest even, saturating at 6.  Scale bytes
+ * 0..3 hold e + 127, bytes 4..7 are zero.  Parity unpinned beyond the codec
+ * pins: the paper gives no MXFP4 example. */
+void orc_mxfp4_row(const float* xc, uint8_t* codes64, uint8_t* scales8);
+void orc_mxfp4_dequant_row(const uint8_t* codes64, const uint8_t* scales8, double* out);
 
 /* Dequantize one NVFP4 row (128 values) to FP64: t * dec(s_g) * dec(q). */
 void orc_nvfp4_dequant_row(const uint8_t* codes64, const uint8_t* scales8, double t,

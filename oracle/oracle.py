@@ -20,6 +20,7 @@ SRC = os.path.join(HERE, "mpfa_oracle.c")
 SMOOTH = 1
 COMPUTE_STATS = 2
 TSCALE_UNIT = 4
+MXFP4 = 8
 QUANT_P = 1
 REVERSE = 2
 
@@ -86,6 +87,10 @@ def lib():
         L.orc_nvfp4_row.argtypes = [C.c_void_p, C.c_float, C.c_void_p, C.c_void_p]
         L.orc_nvfp4_dequant_row.restype = None
         L.orc_nvfp4_dequant_row.argtypes = [C.c_void_p, C.c_void_p, C.c_double, C.c_void_p]
+        L.orc_mxfp4_row.restype = None
+        L.orc_mxfp4_row.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
+        L.orc_mxfp4_dequant_row.restype = None
+        L.orc_mxfp4_dequant_row.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
         L.orc_stats_one.restype = None
         L.orc_stats_one.argtypes = [C.c_void_p, C.c_int64, C.c_int64, C.c_int, C.c_int,
                                     C.c_void_p, C.c_void_p]
@@ -172,6 +177,24 @@ def nvfp4_row(xc, t: float):
     scales = np.empty(8, np.uint8)
     lib().orc_nvfp4_row(_p(xc), float(t), _p(codes), _p(scales))
     return codes, scales
+
+
+def mxfp4_row(xc):
+    """MXFP4 codes (64 bytes) and scale bytes (8; 0..3 used) of one centered row."""
+    xc = _c(xc, np.float32)
+    assert xc.shape == (D,)
+    codes = np.empty(64, np.uint8)
+    scales = np.empty(8, np.uint8)
+    lib().orc_mxfp4_row(_p(xc), _p(codes), _p(scales))
+    return codes, scales
+
+
+def mxfp4_dequant_row(codes, scales) -> np.ndarray:
+    codes = _c(codes, np.uint8)
+    scales = _c(scales, np.uint8)
+    out = np.empty(D, np.float64)
+    lib().orc_mxfp4_dequant_row(_p(codes), _p(scales), _p(out))
+    return out
 
 
 def nvfp4_dequant_row(codes, scales, t: float) -> np.ndarray:
@@ -292,13 +315,13 @@ def _cache_struct(cache, page_table, kv_len, k_tscale, q_codes, q_scales, q_tsca
 
 
 def prefill(cache, page_table, kv_len, k_tscale, q_codes, q_scales, q_tscale, cu_seqlens,
-            q_start, items, smooth=True):
+            q_start, items, smooth=True, mxfp4=False):
     """items: int32 [n][3] rows of (sequence, row within sequence, q head).
     Returns (bf16 bits [n][128], float64 [n][128])."""
     keep = []
     h_q = q_codes.shape[1]
     cs = _cache_struct(cache, page_table, kv_len, k_tscale, q_codes, q_scales, q_tscale, h_q,
-                       SMOOTH if smooth else 0, keep)
+                       (SMOOTH if smooth else 0) | (MXFP4 if mxfp4 else 0), keep)
     items = _c(items, np.int32).reshape(-1, 3)
     ib, ir, ih = (np.ascontiguousarray(items[:, i]) for i in range(3))
     cu = _c(cu_seqlens, np.int32)
@@ -313,12 +336,12 @@ def prefill(cache, page_table, kv_len, k_tscale, q_codes, q_scales, q_tscale, cu
 
 
 def decode(cache, page_table, kv_len, k_tscale, q_codes, q_scales, q_tscale, partition_tokens,
-           items, smooth=True):
+           items, smooth=True, mxfp4=False):
     """items: int32 [n][2] rows of (sequence, q head); q_codes indexed by sequence."""
     keep = []
     h_q = q_codes.shape[1]
     cs = _cache_struct(cache, page_table, kv_len, k_tscale, q_codes, q_scales, q_tscale, h_q,
-                       SMOOTH if smooth else 0, keep)
+                       (SMOOTH if smooth else 0) | (MXFP4 if mxfp4 else 0), keep)
     items = _c(items, np.int32).reshape(-1, 2)
     ib, ih = (np.ascontiguousarray(items[:, i]) for i in range(2))
     n = items.shape[0]

@@ -363,3 +363,88 @@ def test_compensation_lowers_error(orc):
         wins += errs[0] < errs[1]
         ratios.append(errs[0] / errs[1])
     assert wins >= 11 and np.mean(ratios) < 0.8, ratios
+
+
+# ---------------------------------------------------------------------------
+# MXFP4 variant (Sec. 2.1: the 32-element E8M0 block format next to NVFP4)
+# ---------------------------------------------------------------------------
+E2M1_GRID = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+
+
+def _mx_brute(y):
+    """Nearest E2M1 code to y by search over the grid, ties to the even code,
+    magnitudes above 6 clipped (the MX conversion saturates)."""
+    a = min(abs(float(y)), 6.0)
+    d = np.abs(E2M1_GRID - a)
+    cand = np.flatnonzero(d == d.min())
+    mag = int(cand[0]) if len(cand) == 1 else int([c for c in cand if c % 2 == 0][0])
+    return mag | (8 if math.copysign(1.0, float(y)) < 0 else 0)
+
+
+def test_mxfp4_block_rule_brute_force(orc):
+    """Per 32-channel block: X = 2^(floor(log2 amax) - 2), so amax / X lies in
+    [4, 8); every code equals the brute-force nearest grid value of x / X."""
+    rng = np.random.default_rng(7)
+    for trial in range(200):
+        x = (rng.standard_normal(128) * rng.lognormal(0, 3)).astype(np.float32)
+        if trial % 4 == 0:
+            x[rng.integers(0, 128, 2)] *= 50
+        codes, scales = orc.mxfp4_row(x)
+        assert np.all(scales[4:] == 0)
+        nib = np.stack([codes & 15, codes >> 4], 1).reshape(-1)
+        for g in range(4):
+            blk = x[32 * g:32 * g + 32].astype(np.float64)
+            amax = np.abs(blk).max()
+            e = int(scales[g]) - 127
+            assert 4.0 <= amax / 2.0 ** e < 8.0, (trial, g)
+            for i in range(32):
+                assert nib[32 * g + i] == _mx_brute(blk[i] / 2.0 ** e), (trial, g, i)
+
+
+def test_mxfp4_exact_values_round_trip_and_zero_block(orc):
+    """Values already on the scaled E2M1 grid come back exactly; an all-zero
+    block gets the smallest scale and keeps the signs of its zeros."""
+    rng = np.random.default_rng(8)
+    x = np.zeros(128, np.float32)
+    for g in range(3):
+        e = int(rng.integers(-20, 20))
+        vals = rng.choice(E2M1_GRID, 32) * rng.choice([-1, 1], 32)
+        vals[0] = 6.0                                  # the block maximum fixes X = 2^e
+        x[32 * g:32 * g + 32] = (vals * 2.0 ** e).astype(np.float32)
+    x[96:] = 0.0
+    x[100] = -0.0
+    codes, scales = orc.mxfp4_row(x)
+    deq = orc.mxfp4_dequant_row(codes, scales)
+    assert np.array_equal(deq[:96], x[:96].astype(np.float64))
+    assert scales[3] == 0 and np.all(deq[96:] == 0)
+    assert (codes[50] >> 0) & 15 == 8                   # channel 100: -0 keeps its sign
+
+
+def test_mxfp4_prefill_matches_dequantized_reference(orc):
+    """With Q and K in MXFP4 the attention equals FP64 attention over the
+    dequantized values (same tiles, same P quantization), and the tensor
+    scales are 1."""
+    n = 200
+    g = W.gen_qkv(31, [n], 2, 1, True, "cpu")
+    qb, kb, vb = (W.bits(t) for t in g)
+    r = orc.quantize_qk(qb, kb, vb, [0, n], np.arange(n, dtype=np.int64), 4,
+                        orc.SMOOTH | orc.COMPUTE_STATS | orc.MXFP4)
+    assert np.all(r["q_tscale"] == 1.0) and np.all(r["k_tscale"] == 1.0)
+    items = np.array([(0, i, h) for i in range(0, n, 7) for h in range(2)], np.int32)
+    a, a64 = orc.prefill(r["cache"], np.arange(4, dtype=np.int32)[None], [n], r["k_tscale"],
+                         r["q_codes"], r["q_scales"], r["q_tscale"], [0, n], [0], items,
+                         mxfp4=True)
+    kc, ks, vc, ds = (r["cache"][x] for x in ("k_codes", "k_scales", "v_codes", "ds"))
+    kd = np.stack([orc.mxfp4_dequant_row(kc[j // 64, 0, j % 64], ks[j // 64, 0, j % 64])
+                   for j in range(n)])
+    vd = np.stack([[orc.e4m3_value(int(vc[j // 64, 0, c, j % 64])) for c in range(128)]
+                   for j in range(n)])
+    for h in range(2):
+        qd = np.stack([orc.mxfp4_dequant_row(r["q_codes"][i, h], r["q_scales"][i, h])
+                       for i in range(n)])
+        dsd = bits_to_f64(ds[:, h, :].reshape(-1)[:n])
+        sel = items[:, 2] == h
+        rows = items[sel, 1]
+        ref = orc.attention_f64(qd[rows], kd, vd, np.tile(dsd, (len(rows), 1)), rows,
+                                tile=128, flags=orc.REVERSE | orc.QUANT_P)
+        assert np.max(np.abs(a64[sel] - ref)) < 1e-12
