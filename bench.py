@@ -83,6 +83,7 @@ def parse():
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-direct", action="store_true", help="skip the unsmoothed prefill variant")
+    ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=16384, help="oracle sample: query rows of head 0")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -110,7 +111,7 @@ class Timer:
         return self.s.elapsed_time(self.e)
 
 
-def setup_prefill(torch, np, mp, W, seq, smooth):
+def setup_prefill(torch, np, mp, W, seq, smooth, mx=False):
     wl = W.qwen_prefill(seq)
     dev = "cuda"
     q, k, v = W.gen_qkv(wl.seed, [seq], wl.h_q, wl.h_kv, wl.outliers, dev)
@@ -123,7 +124,7 @@ def setup_prefill(torch, np, mp, W, seq, smooth):
               cache=mp.PagedCache(n_pages, wl.h_q, wl.h_kv, dev, smooth=smooth),
               stats=mp.SeqStats(1, wl.h_q, wl.h_kv, dev), qq=mp.QuantQ(seq, 1, wl.h_q, dev),
               out=torch.empty((seq, wl.h_q, 128), dtype=torch.bfloat16, device=dev),
-              flags=(mp.SMOOTH if smooth else 0))
+              flags=(mp.SMOOTH if smooth else 0) | (mp.MXFP4 if mx else 0))
     return st
 
 
@@ -137,9 +138,10 @@ def run_prefill(mp, st):
                st["pt_d"], st["out"], st["q"].shape[0], st["flags"])
 
 
-def setup_decode(torch, np, mp, W, batch):
+def setup_decode(torch, np, mp, W, batch, mx=False):
     wl = W.llama_decode(batch)
     dev = "cuda"
+    fmt = mp.MXFP4 if mx else 0
     lens = wl.kv_len
     pt, n_pages = W.make_pages(wl.seed, lens)
     cache = mp.PagedCache(n_pages, wl.h_q, wl.h_kv, dev)
@@ -153,7 +155,7 @@ def setup_decode(torch, np, mp, W, batch):
         qq = mp.QuantQ(ctx, 1, wl.h_q, dev)
         slots = W.slots_for(pt, b, range(ctx))
         mp.quantize_qk(q, k, v, d(np.array([0, ctx], np.int32)), d(slots), cache, sb, qq,
-                       mp.SMOOTH | mp.COMPUTE_STATS, ctx)
+                       mp.SMOOTH | mp.COMPUTE_STATS | fmt, ctx)
         stats.q_mean[b].copy_(sb.q_mean[0])
         stats.k_mean[b].copy_(sb.k_mean[0])
         stats.k_tscale[b].copy_(sb.k_tscale[0])
@@ -165,7 +167,7 @@ def setup_decode(torch, np, mp, W, batch):
     slots1 = np.array([W.slots_for(pt, b, [lens[b] - 1])[0] for b in range(batch)], np.int64)
     qq = mp.QuantQ(batch, batch, wl.h_q, dev)
     mp.quantize_qk(qn, kn, vn, d(np.arange(batch + 1, dtype=np.int32)), d(slots1), cache,
-                   stats, qq, mp.SMOOTH, 1)
+                   stats, qq, mp.SMOOTH | fmt, 1)
     part = mp.decode_choose_partition(lens, wl.h_kv, torch.cuda.get_device_properties(0).multi_processor_count)
     maxp = max(math.ceil(n / part) for n in lens)
     ws = torch.empty(mp.decode_workspace_size(batch, wl.h_q, maxp) // 4, dtype=torch.float32,
@@ -173,12 +175,13 @@ def setup_decode(torch, np, mp, W, batch):
     out = torch.empty((batch, wl.h_q, 128), dtype=torch.bfloat16, device=dev)
     torch.cuda.synchronize()
     return dict(wl=wl, lens=lens, pt=pt, pt_d=d(pt), cache=cache, stats=stats, qq=qq, ws=ws,
-                out=out, kv_len=d(np.asarray(lens, np.int32)), part=part, maxp=maxp)
+                out=out, kv_len=d(np.asarray(lens, np.int32)), part=part, maxp=maxp,
+                flags=mp.SMOOTH | fmt, mx=mx)
 
 
 def run_decode(mp, st):
     mp.decode_paged(st["qq"], st["cache"], st["stats"], st["kv_len"], st["pt_d"], st["out"],
-                    st["part"], st["maxp"], st["ws"], mp.SMOOTH)
+                    st["part"], st["maxp"], st["ws"], st["flags"])
 
 
 def decode_bytes(st):
@@ -186,7 +189,8 @@ def decode_bytes(st):
     every key, the quantized queries, the outputs, the page-table entries."""
     wl = st["wl"]
     keys = sum(st["lens"])
-    per_key = wl.h_kv * (64 + 8 + 128) + wl.h_q * 2
+    scale_bytes = 4 if st.get("mx") else 8       # MXFP4 reads scale bytes 0..3 only
+    per_key = wl.h_kv * (64 + scale_bytes + 128) + wl.h_q * 2
     pages = sum(math.ceil(n / 64) for n in st["lens"])
     return keys * per_key + wl.batch * wl.h_q * (72 + 4) + wl.batch * wl.h_q * 256 + pages * 4 \
         + wl.batch * 4
@@ -302,6 +306,29 @@ def main():
             res["cpu_baseline"] = cpu_baseline(np, W, st, args.cpu_rows)
         del st
         torch.cuda.empty_cache()
+        if not args.no_mxfp4:
+            log("prefill, MXFP4 variant (E8M0 per 32, QK on the scaled FP4 MFMA) ...")
+            sm = setup_prefill(torch, np, mp, W, seq, smooth=True, mx=True)
+            for _ in range(args.warmup):
+                run_quant(mp, sm)
+                run_prefill(mp, sm)
+            torch.cuda.synchronize()
+            qt, ts = [], []
+            for _ in range(args.steps):
+                with Timer(torch) as t1:
+                    run_quant(mp, sm)
+                with Timer(torch) as t2:
+                    run_prefill(mp, sm)
+                qt.append(t1)
+                ts.append(t2)
+            torch.cuda.synchronize()
+            mx_ms = sum(t.ms() for t in ts) / args.steps
+            mx_tf = flops / (mx_ms * 1e-3)
+            res["prefill_mxfp4"] = {"ms": mx_ms, "tflops": mx_tf / 1e12,
+                                    "frac_fp4_fp8_peak": mx_tf / peak,
+                                    "quant_ms": sum(t.ms() for t in qt) / args.steps}
+            del sm
+            torch.cuda.empty_cache()
 
     if not args.no_decode:
         log(f"setup decode batch {args.decode_batch} ...")
@@ -322,6 +349,26 @@ def main():
                          "bytes": nbytes, "traffic": measured_traffic("decode_kernel"),
                          "partition_tokens": sd["part"],
                          "keys": int(sum(sd["lens"]))}
+        del sd
+        torch.cuda.empty_cache()
+        if not args.no_mxfp4:
+            log("decode, MXFP4 variant ...")
+            sx = setup_decode(torch, np, mp, W, args.decode_batch, mx=True)
+            for _ in range(args.warmup):
+                run_decode(mp, sx)
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(args.steps):
+                with Timer(torch) as t:
+                    run_decode(mp, sx)
+                ts.append(t)
+            torch.cuda.synchronize()
+            mx_ms = sum(t.ms() for t in ts) / args.steps
+            mx_bytes = decode_bytes(sx)
+            res["decode_mxfp4"] = {"ms": mx_ms, "GB/s": mx_bytes / (mx_ms * 1e-3) / 1e9,
+                                   "frac_hbm": mx_bytes / (mx_ms * 1e-3) / PEAK_HBM,
+                                   "bytes": mx_bytes}
+            del sx
 
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")

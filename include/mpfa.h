@@ -79,6 +79,11 @@ typedef enum {
 #define MPFA_SEED_INIT     8u  /* prefill: load the rank-one term 1 Delta_S^T as the input
                                   accumulator of the first QK MFMA instead of issuing the
                                   BF16 rank-one MFMA; results are bit-identical            */
+#define MPFA_MXFP4        16u  /* Q/K in MXFP4 instead of NVFP4 (quantize, prefill, decode):
+                                  one E8M0 scale per 32 channels (scale bytes 0..3 of the
+                                  8-byte scale row; bytes 4..7 zero), tensor scales 1, and
+                                  QK on the scaled FP4 MFMA.  All calls on one cache must
+                                  agree on this flag.                                      */
 
 /* ------------------------------------------------------------------------ */
 /* Quantization / cache-write pass (Algorithm 1 stage one; Sec. 4.2, 4.3, 6) */
@@ -97,6 +102,10 @@ typedef enum {
  *  - Q_c = Q - Qbar and K_c = K - Kbar in FP32; NVFP4 per 16-channel group:
  *    scale = E4M3_RNE_sat(amax / (6 t)), codes = E2M1_RNE_sat(x / (t * scale))
  *    with IEEE FP32 divisions; a group whose scale is 0 stores sign-only codes.
+ *  - With MPFA_MXFP4 (the 32-element E8M0 block format Sec. 2.1 names next to
+ *    NVFP4): tensor scales are 1; per 32-channel block X = 2^e with
+ *    e = floor(log2 amax) - 2 clamped to [-127, 127] (e = -127 for an all-zero
+ *    block), scale byte e + 127, codes = E2M1_RNE_sat(x / X).
  *  - V is stored as E4M3_RNE_sat(V) (no scale, not centered, Sec. 4.2).
  *  - With MPFA_SMOOTH, ds[slot][h_q] = BF16_RNE(sum_c Qbar[h_q][c] * K_c[c])
  *    as an FP32 fused multiply-add chain over c = 0..127 (Eq. 9).
@@ -109,7 +118,7 @@ typedef struct {
     int32_t max_seqlen;       /* host: max tokens of one sequence in this call   */
     int32_t h_q, h_kv;        /* heads; h_q % h_kv == 0, h_q <= MPFA_MAX_HEADS   */
     int32_t head_dim;         /* must be 128                                     */
-    uint32_t flags;           /* MPFA_SMOOTH | MPFA_COMPUTE_STATS | MPFA_TSCALE_UNIT */
+    uint32_t flags;           /* MPFA_SMOOTH | MPFA_COMPUTE_STATS | MPFA_TSCALE_UNIT | MPFA_MXFP4 */
     int64_t num_pages;        /* cache capacity in pages (slot_mapping < 64 * num_pages) */
     const int32_t* cu_seqlens;   /* [batch+1]                                    */
     const void* q;               /* bf16 [T][h_q][128]                           */
@@ -152,7 +161,7 @@ typedef struct {
     int32_t batch, h_q, h_kv, head_dim;
     int32_t max_seqlen_q;     /* host: max query tokens of one sequence          */
     int32_t max_pages;        /* page_table row length                           */
-    uint32_t flags;           /* MPFA_SMOOTH, MPFA_SEED_INIT                     */
+    uint32_t flags;           /* MPFA_SMOOTH, MPFA_SEED_INIT, MPFA_MXFP4         */
     const int32_t* cu_seqlens_q; /* [batch+1] query tokens                       */
     const int32_t* q_start;   /* [batch] absolute position of query 0            */
     const int32_t* kv_len;    /* [batch] keys in the cache (>= q_start + n_q)    */
@@ -192,7 +201,7 @@ typedef struct {
     int32_t max_pages;
     int32_t partition_tokens; /* multiple of 128                                  */
     int32_t max_partitions;   /* >= ceil(max_b kv_len[b] / partition_tokens)      */
-    uint32_t flags;           /* MPFA_SMOOTH                                      */
+    uint32_t flags;           /* MPFA_SMOOTH, MPFA_MXFP4                          */
     const int32_t* kv_len;    /* [batch], each >= 1                               */
     const int32_t* page_table;/* [batch][max_pages]                               */
     const uint8_t* q_codes;   /* [batch][h_q][64]                                 */

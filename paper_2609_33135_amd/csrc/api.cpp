@@ -44,7 +44,8 @@ mpfa_status mpfa_quantize_qk(const mpfa_quant_args* a, mpfa_stream_t stream) {
   if (a->batch < 1 || a->total_tokens < 0 || a->max_seqlen < 0 || a->num_pages < 1)
     return MPFA_ERR_INVALID;
   if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
-  if (a->flags & ~(MPFA_SMOOTH | MPFA_COMPUTE_STATS | MPFA_TSCALE_UNIT)) return MPFA_ERR_INVALID;
+  if (a->flags & ~(MPFA_SMOOTH | MPFA_COMPUTE_STATS | MPFA_TSCALE_UNIT | MPFA_MXFP4))
+    return MPFA_ERR_INVALID;
   const bool smooth = a->flags & MPFA_SMOOTH;
   if (!a->cu_seqlens || !a->q || !a->k || !a->v || !a->slot_mapping || !a->q_mean || !a->k_mean ||
       !a->k_tscale || !a->q_codes || !a->q_scales || !a->q_tscale || !a->k_codes || !a->k_scales ||
@@ -61,6 +62,7 @@ mpfa_status mpfa_quantize_qk(const mpfa_quant_args* a, mpfa_stream_t stream) {
   p.compute_stats = (a->flags & MPFA_COMPUTE_STATS) != 0;
   p.stats_k = p.compute_stats;
   p.tscale_unit = (a->flags & MPFA_TSCALE_UNIT) != 0;
+  p.mx = (a->flags & MPFA_MXFP4) != 0;
   p.cu_seqlens = a->cu_seqlens;
   p.q = static_cast<const uint16_t*>(a->q);
   p.k = static_cast<const uint16_t*>(a->k);
@@ -85,7 +87,7 @@ mpfa_status mpfa_prefill(const mpfa_prefill_args* a, mpfa_stream_t stream) {
   if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
   if (a->batch < 1 || a->max_seqlen_q < 0 || a->max_pages < 1) return MPFA_ERR_INVALID;
   if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
-  if (a->flags & ~(MPFA_SMOOTH | MPFA_SEED_INIT)) return MPFA_ERR_INVALID;
+  if (a->flags & ~(MPFA_SMOOTH | MPFA_SEED_INIT | MPFA_MXFP4)) return MPFA_ERR_INVALID;
   const bool smooth = a->flags & MPFA_SMOOTH;
   if (!a->cu_seqlens_q || !a->q_start || !a->kv_len || !a->page_table || !a->q_codes ||
       !a->q_scales || !a->q_tscale || !a->k_codes || !a->k_scales || !a->v_codes ||
@@ -102,6 +104,7 @@ mpfa_status mpfa_prefill(const mpfa_prefill_args* a, mpfa_stream_t stream) {
   p.n_qtiles = (int)n_qtiles;
   p.smooth = smooth;
   p.seed_init = (a->flags & MPFA_SEED_INIT) != 0;
+  p.mx = (a->flags & MPFA_MXFP4) != 0;
   p.xcd_remap = (a->h_kv % 8) == 0;
   p.lam = kLambda;
   p.cu_seqlens_q = a->cu_seqlens_q;
@@ -156,7 +159,7 @@ mpfa_status mpfa_decode_paged(const mpfa_decode_args* a, void* workspace, size_t
     return MPFA_ERR_INVALID;
   if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
   if (a->h_q / a->h_kv > kMaxDecodeGroup) return MPFA_ERR_UNSUPPORTED;
-  if (a->flags & ~MPFA_SMOOTH) return MPFA_ERR_INVALID;
+  if (a->flags & ~(MPFA_SMOOTH | MPFA_MXFP4)) return MPFA_ERR_INVALID;
   const bool smooth = a->flags & MPFA_SMOOTH;
   if (!a->kv_len || !a->page_table || !a->q_codes || !a->q_scales || !a->q_tscale ||
       !a->k_codes || !a->k_scales || !a->v_codes || !a->k_tscale || !a->out || (smooth && !a->ds))
@@ -174,6 +177,7 @@ mpfa_status mpfa_decode_paged(const mpfa_decode_args* a, void* workspace, size_t
   p.partition_tokens = a->partition_tokens;
   p.max_partitions = a->max_partitions;
   p.smooth = smooth;
+  p.mx = (a->flags & MPFA_MXFP4) != 0;
   p.lam = kLambda;
   p.kv_len = a->kv_len;
   p.page_table = a->page_table;

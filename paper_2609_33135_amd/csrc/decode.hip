@@ -36,7 +36,7 @@ typedef __attribute__((address_space(1))) void* global_ptr_t;
 // LDS V layout: for channel block db and half hf, the 1 KB slab at
 // (2 db + hf) KB holds, at 16 * lane, the bytes the lane feeds to the MFMA:
 // channel 16 db + lane%16, keys 32 (lane/16) + 16 hf .. +15.
-template <bool SMOOTH>
+template <bool SMOOTH, bool MX>
 __global__ __launch_bounds__(kWavesPerBlock * 64, 2) void decode_kernel(DecodeParams p) {
   __shared__ __attribute__((aligned(16))) uint8_t vlds[kWavesPerBlock * kVBytes];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 4, lr = lane & 15;
@@ -59,18 +59,26 @@ __global__ __launch_bounds__(kWavesPerBlock * 64, 2) void decode_kernel(DecodePa
   const float lam2 = __builtin_ldexpf(p.lam, eqk);           // per query head (column lr)
   const float seed_scale = __builtin_ldexpf(1.0f, -eqk);     // Delta_S in accumulator units
 
-  // Q operand: column lr = query head hk*G + lr; channels 32g + 8ks + e
+  // Q operand: column lr = query head hk*G + lr; channels 32g .. 32g+31 (NVFP4:
+  // dequantized to FP16 in four 8-channel slices; MXFP4: the raw codes)
   f16x8 qop[4];
+  u32x4 qraw;
+  int qscale = 0;
   {
     const uint8_t* qc = p.q_codes + ((int64_t)b * p.h_q + h) * 64;
     const uint8_t* qsc = p.q_scales + ((int64_t)b * p.h_q + h) * 8;
     const u32x4 cw = qvalid ? *reinterpret_cast<const u32x4*>(qc + 16 * g) : (u32x4){0u, 0u, 0u, 0u};
-    const uint32_t sc = qvalid ? *reinterpret_cast<const uint16_t*>(qsc + 2 * g) : 0u;
-    const ScaleSplit s0 = split_e4m3(sc & 0xFFu), s1 = split_e4m3((sc >> 8) & 0xFFu);
-    qop[0] = dequant8(cw[0], s0);
-    qop[1] = dequant8(cw[1], s0);
-    qop[2] = dequant8(cw[2], s1);
-    qop[3] = dequant8(cw[3], s1);
+    if (MX) {
+      qraw = cw;
+      qscale = qvalid ? qsc[g] : 127;
+    } else {
+      const uint32_t sc = qvalid ? *reinterpret_cast<const uint16_t*>(qsc + 2 * g) : 0u;
+      const ScaleSplit s0 = split_e4m3(sc & 0xFFu), s1 = split_e4m3((sc >> 8) & 0xFFu);
+      qop[0] = dequant8(cw[0], s0);
+      qop[1] = dequant8(cw[1], s0);
+      qop[2] = dequant8(cw[2], s1);
+      qop[3] = dequant8(cw[3], s1);
+    }
   }
 
   const int krow_in_tile = 32 * (lr >> 2) + (lr & 3);   // + 4 mb: key of MFMA row lr
@@ -92,7 +100,8 @@ __global__ __launch_bounds__(kWavesPerBlock * 64, 2) void decode_kernel(DecodePa
     for (int mb = 0; mb < 8; ++mb) {
       const int64_t row = kpage * page_k_rows + kv_head + ((krow_in_tile + 4 * mb) & 63);
       kc[mb] = *reinterpret_cast<const u32x4*>(p.k_codes + row * 64 + 16 * g);
-      ksc[mb] = *reinterpret_cast<const uint16_t*>(p.k_scales + row * 8 + 2 * g);
+      ksc[mb] = MX ? (uint32_t)p.k_scales[row * 8 + g]
+                   : (uint32_t)*reinterpret_cast<const uint16_t*>(p.k_scales + row * 8 + 2 * g);
     }
     // compensation of the lane's accumulator rows: keys 32g + 4mb .. +3, head lr
     if (SMOOTH) {
@@ -175,11 +184,15 @@ __global__ __launch_bounds__(kWavesPerBlock * 64, 2) void decode_kernel(DecodePa
       f32x4 c = (f32x4){__uint_as_float(dsw[mb].x << 16), __uint_as_float(dsw[mb].x & 0xFFFF0000u),
                         __uint_as_float(dsw[mb].y << 16), __uint_as_float(dsw[mb].y & 0xFFFF0000u)};
       c *= seed_scale;   // exact: power of two
-      const ScaleSplit s0 = split_e4m3(ksc[mb] & 0xFFu), s1 = split_e4m3((ksc[mb] >> 8) & 0xFFu);
-      c = mfma_f16(dequant8(kc[mb][0], s0), qop[0], c);
-      c = mfma_f16(dequant8(kc[mb][1], s0), qop[1], c);
-      c = mfma_f16(dequant8(kc[mb][2], s1), qop[2], c);
-      s[mb] = mfma_f16(dequant8(kc[mb][3], s1), qop[3], c);
+      if (MX) {
+        s[mb] = mfma_fp4(kc[mb], qraw, c, (int)ksc[mb], qscale);
+      } else {
+        const ScaleSplit s0 = split_e4m3(ksc[mb] & 0xFFu), s1 = split_e4m3((ksc[mb] >> 8) & 0xFFu);
+        c = mfma_f16(dequant8(kc[mb][0], s0), qop[0], c);
+        c = mfma_f16(dequant8(kc[mb][1], s0), qop[1], c);
+        c = mfma_f16(dequant8(kc[mb][2], s1), qop[2], c);
+        s[mb] = mfma_f16(dequant8(kc[mb][3], s1), qop[3], c);
+      }
     }
     if (j > j_lo) load_k(j - 1);
     if (key0 + kTile > kend) {
@@ -263,10 +276,14 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeParams p) {
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
   if (p.batch == 0) return hipSuccess;
   const dim3 grid((p.max_partitions + kWavesPerBlock - 1) / kWavesPerBlock, p.h_kv, p.batch);
-  if (p.smooth)
-    decode_kernel<true><<<grid, dim3(kWavesPerBlock * 64), 0, stream>>>(p);
-  else
-    decode_kernel<false><<<grid, dim3(kWavesPerBlock * 64), 0, stream>>>(p);
+  const dim3 block(kWavesPerBlock * 64);
+  if (p.mx) {
+    if (p.smooth) decode_kernel<true, true><<<grid, block, 0, stream>>>(p);
+    else decode_kernel<false, true><<<grid, block, 0, stream>>>(p);
+  } else {
+    if (p.smooth) decode_kernel<true, false><<<grid, block, 0, stream>>>(p);
+    else decode_kernel<false, false><<<grid, block, 0, stream>>>(p);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   merge_kernel<<<dim3(p.h_q, p.batch), dim3(128), 0, stream>>>(p);

@@ -139,6 +139,15 @@ __device__ __forceinline__ f32x4 mfma_fp8(i32x8 a, i32x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0x7F7F7F7F, 0, 0x7F7F7F7F);
 }
 
+// Scaled FP4 MFMA (MXFP4): A and B hold 32 E2M1 values per lane (16 bytes in
+// the low four registers, element 2j in the low nibble of byte j), each lane
+// with its own E8M0 scale byte for its 32-element block.
+__device__ __forceinline__ f32x4 mfma_fp4(u32x4 a, u32x4 b, f32x4 c, int scale_a, int scale_b) {
+  const i32x8 av = {(int)a[0], (int)a[1], (int)a[2], (int)a[3], 0, 0, 0, 0};
+  const i32x8 bv = {(int)b[0], (int)b[1], (int)b[2], (int)b[3], 0, 0, 0, 0};
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(av, bv, c, 4, 4, 0, scale_a, 0, scale_b);
+}
+
 // Four FP32 values in [0, 448] -> four E4M3 bytes (hardware RNE).
 __device__ __forceinline__ uint32_t pack_fp8x4(float a, float b, float c, float d) {
   int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);

@@ -12,6 +12,7 @@ constexpr int kMaxKvHeadsQuant = 32;
 struct QuantParams {
   int batch, total_tokens, h_q, h_kv;
   int smooth, compute_stats, stats_k, tscale_unit;
+  int mx;           // Q/K in MXFP4 (E8M0 per 32 channels, tensor scale 1)
   const int32_t* cu_seqlens;
   const uint16_t* q;
   const uint16_t* k;
@@ -34,6 +35,7 @@ struct PrefillParams {
   int n_qtiles;     // max query tiles of one sequence
   int smooth;
   int seed_init;    // 1: compensation loaded as the accumulator input, 0: rank-one MFMA
+  int mx;           // Q/K in MXFP4: QK on the scaled FP4 MFMA
   int xcd_remap;    // 1: spread KV heads over the 8 XCDs (needs h_kv % 8 == 0)
   float lam;        // log2(e) / sqrt(128)
   const int32_t* cu_seqlens_q;
@@ -55,6 +57,7 @@ struct DecodeParams {
   int batch, h_q, h_kv, max_pages;
   int partition_tokens, max_partitions;
   int smooth;
+  int mx;           // Q/K in MXFP4: QK on the scaled FP4 MFMA
   float lam;
   const int32_t* kv_len;
   const int32_t* page_table;

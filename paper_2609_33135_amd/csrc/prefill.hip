@@ -31,7 +31,10 @@ constexpr int kQRows = kWaves * kNB * 16;    // 256 query rows per workgroup
 constexpr int kThreads = kWaves * 64;
 
 struct PrefillSmem {
-  uint8_t k[kTile * 256];   // FP16 [key][128], 16-byte chunks XOR-swizzled per key
+  // NVFP4: FP16 [key][128], 16-byte chunks XOR-swizzled per key.  MXFP4: raw
+  // codes [key][64] (chunks swizzled by mx_swz) in the first 8 KB, then the
+  // E8M0 scales transposed to [MFMA row][32-channel block][16-key block].
+  uint8_t k[kTile * 256];
   uint8_t v[kD * kTile];    // FP8 [channel][key], 16-byte chunks XOR-swizzled per channel
   uint16_t ds[kTile];       // BF16 seed values in accumulator units
 };
@@ -39,6 +42,8 @@ struct PrefillSmem {
 // chunk swizzles: conflict-free 16-byte reads for the MFMA operand patterns
 __device__ __forceinline__ int k_swz(int key) { return (((key >> 5) << 2) | (key & 3)) & 15; }
 __device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 7; }
+__device__ __forceinline__ int mx_swz(int key) { return ((key >> 1) & 1) | (((key >> 5) & 1) << 1); }
+constexpr int kMxScaleOff = kTile * 64;   // byte offset of the MXFP4 scales in PrefillSmem::k
 
 __device__ __forceinline__ u32x4 zero_tail(u32x4 w, int nvalid) {
   // keep bytes [0, nvalid) of the 16-byte word
@@ -61,6 +66,7 @@ struct TileRegs {
   uint32_t ds;     // BF16 Delta_S of key t (threads 0..127)
 };
 
+template <bool MX>
 __device__ __forceinline__ void fetch_tile(TileRegs& r, const PrefillParams& p, const int32_t* pt,
                                            int hk, int h, int j, int kvl) {
   const int t = threadIdx.x;
@@ -76,7 +82,8 @@ __device__ __forceinline__ void fetch_tile(TileRegs& r, const PrefillParams& p, 
     r.ksc = 0;
     if (kabs < kvl) {
       r.kc = *reinterpret_cast<const u32x4*>(p.k_codes + row * 64 + qt * 16);
-      r.ksc = *reinterpret_cast<const uint16_t*>(p.k_scales + row * 8 + qt * 2);
+      r.ksc = MX ? (uint32_t)p.k_scales[row * 8 + qt]
+                 : (uint32_t)*reinterpret_cast<const uint16_t*>(p.k_scales + row * 8 + qt * 2);
     }
   }
   {
@@ -103,9 +110,16 @@ __device__ __forceinline__ void fetch_tile(TileRegs& r, const PrefillParams& p, 
   }
 }
 
+template <bool MX>
 __device__ __forceinline__ void store_tile(PrefillSmem& sm, const TileRegs& r, float seed_scale) {
   const int t = threadIdx.x;
-  {
+  if (MX) {
+    const int key = t >> 2, qt = t & 3;
+    *reinterpret_cast<u32x4*>(sm.k + key * 64 + ((qt ^ mx_swz(key)) << 4)) = r.kc;
+    // key -> MFMA row 4*(key/32) + key%4 of 16-key block (key/4)%8
+    const int mrow = 4 * (key >> 5) + (key & 3), mblk = (key >> 2) & 7;
+    sm.k[kMxScaleOff + (mrow * 4 + qt) * 8 + mblk] = (uint8_t)r.ksc;
+  } else {
     const int key = t >> 2, qt = t & 3;
     const ScaleSplit s0 = split_e4m3(r.ksc & 0xFFu), s1 = split_e4m3((r.ksc >> 8) & 0xFFu);
     uint8_t* rowp = sm.k + key * 256;
@@ -137,7 +151,7 @@ __device__ __forceinline__ void store_tile(PrefillSmem& sm, const TileRegs& r, f
 //  kSeedNone  no compensation (the unsmoothed "direct" variant).
 enum SeedMode { kSeedNone = 0, kSeedMfma = 1, kSeedInit = 2 };
 
-template <int SEED>
+template <int SEED, bool MX>
 __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   __shared__ __attribute__((aligned(16))) PrefillSmem smem[2];
 
@@ -187,8 +201,12 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   const int wpos_min = qs + wrow0;
   const int wpos_max = qs + min(wrow0 + kNB * 16, nq) - 1;
 
-  // ---- Q operands (B of S^T = K Q^T): exact FP16, tensor scale factored out
+  // ---- Q operands (B of S^T = K Q^T).  NVFP4: exact FP16, tensor scale
+  // factored out.  MXFP4: the raw codes of channels 32g .. 32g+31 and their
+  // E8M0 scale (the lane's 32-element block of the scaled FP4 MFMA).
   f16x8 qop[kNB][4];
+  u32x4 qraw[kNB];
+  int qscale[kNB];
   int pos[kNB];
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
@@ -198,11 +216,16 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
     const int64_t tok = q0 + (valid ? row : 0);
     const uint8_t* qc = p.q_codes + (tok * p.h_q + h) * 64;
     const uint8_t* qsc = p.q_scales + (tok * p.h_q + h) * 8;
+    if (MX) {
+      qraw[nb] = valid ? *reinterpret_cast<const u32x4*>(qc + 16 * g) : (u32x4){0u, 0u, 0u, 0u};
+      qscale[nb] = valid ? qsc[g] : 127;
+    } else {
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const uint32_t cw = valid ? *reinterpret_cast<const uint32_t*>(qc + 16 * ks + 4 * g) : 0u;
-      const uint32_t sc = valid ? qsc[2 * ks + (g >> 1)] : 0u;
-      qop[nb][ks] = dequant8(cw, split_e4m3(sc));
+      for (int ks = 0; ks < 4; ++ks) {
+        const uint32_t cw = valid ? *reinterpret_cast<const uint32_t*>(qc + 16 * ks + 4 * g) : 0u;
+        const uint32_t sc = valid ? qsc[2 * ks + (g >> 1)] : 0u;
+        qop[nb][ks] = dequant8(cw, split_e4m3(sc));
+      }
     }
   }
 
@@ -222,13 +245,13 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   const int32_t* pt = p.page_table + (int64_t)b * p.max_pages;
   {
     TileRegs r0r;
-    fetch_tile(r0r, p, pt, hk, h, j_hi, kvl);
-    store_tile(smem[j_hi & 1], r0r, seed_scale);
+    fetch_tile<MX>(r0r, p, pt, hk, h, j_hi, kvl);
+    store_tile<MX>(smem[j_hi & 1], r0r, seed_scale);
   }
   __syncthreads();
   for (int j = j_hi; j >= 0; --j) {
     TileRegs nxt;
-    if (j > 0) fetch_tile(nxt, p, pt, hk, h, j - 1, kvl);
+    if (j > 0) fetch_tile<MX>(nxt, p, pt, hk, h, j - 1, kvl);
     const PrefillSmem& sm = smem[j & 1];
     const int key0 = j * kTile;
     if (wave_active && key0 <= wpos_max) {
@@ -251,17 +274,30 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = seed;
       }
+      if (MX) {
+        // one scaled FP4 MFMA per 16x16 block covers all 128 channels
+        const uint64_t ks8 = *reinterpret_cast<const uint64_t*>(sm.k + kMxScaleOff + (lr * 4 + g) * 8);
 #pragma unroll
-      for (int half = 0; half < 2; ++half)
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-        for (int mb = 4 * half; mb < 4 * half + 4; ++mb) {
+        for (int mb = 0; mb < 8; ++mb) {
           const int krow = 32 * (lr >> 2) + 4 * mb + (lr & 3);
-          const f16x8 kop = *reinterpret_cast<const f16x8*>(sm.k + krow * 256 + (((4 * ks + g) ^ lr) << 4));
+          const u32x4 kop = *reinterpret_cast<const u32x4*>(sm.k + krow * 64 + ((g ^ mx_swz(krow)) << 4));
+          const int sk = (int)((ks8 >> (8 * mb)) & 0xFFu);
 #pragma unroll
-          for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_f16(kop, qop[nb][ks], s[mb][nb]);
+          for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_fp4(kop, qraw[nb], s[mb][nb], sk, qscale[nb]);
         }
+      } else {
+#pragma unroll
+        for (int half = 0; half < 2; ++half)
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+            for (int mb = 4 * half; mb < 4 * half + 4; ++mb) {
+              const int krow = 32 * (lr >> 2) + 4 * mb + (lr & 3);
+              const f16x8 kop = *reinterpret_cast<const f16x8*>(sm.k + krow * 256 + (((4 * ks + g) ^ lr) << 4));
+#pragma unroll
+              for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_f16(kop, qop[nb][ks], s[mb][nb]);
+            }
+          }
       }
       if (need_mask) {
 #pragma unroll
@@ -320,7 +356,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
         for (int nb = 0; nb < kNB; ++nb) o[db][nb] = mfma_fp8(vop, pb[nb], o[db][nb]);
       }
     }
-    if (j > 0) store_tile(smem[(j - 1) & 1], nxt, seed_scale);
+    if (j > 0) store_tile<MX>(smem[(j - 1) & 1], nxt, seed_scale);
     __syncthreads();
   }
 
@@ -350,12 +386,16 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream) {
   const unsigned blocks = (unsigned)(p.n_qtiles * p.h_q * p.batch);
   if (blocks == 0) return hipSuccess;
-  if (!p.smooth)
-    prefill_kernel<kSeedNone><<<dim3(blocks), dim3(kThreads), 0, stream>>>(p);
-  else if (p.seed_init)
-    prefill_kernel<kSeedInit><<<dim3(blocks), dim3(kThreads), 0, stream>>>(p);
-  else
-    prefill_kernel<kSeedMfma><<<dim3(blocks), dim3(kThreads), 0, stream>>>(p);
+  const dim3 grid(blocks), block(kThreads);
+  if (p.mx) {
+    if (!p.smooth) prefill_kernel<kSeedNone, true><<<grid, block, 0, stream>>>(p);
+    else if (p.seed_init) prefill_kernel<kSeedInit, true><<<grid, block, 0, stream>>>(p);
+    else prefill_kernel<kSeedMfma, true><<<grid, block, 0, stream>>>(p);
+  } else {
+    if (!p.smooth) prefill_kernel<kSeedNone, false><<<grid, block, 0, stream>>>(p);
+    else if (p.seed_init) prefill_kernel<kSeedInit, false><<<grid, block, 0, stream>>>(p);
+    else prefill_kernel<kSeedMfma, false><<<grid, block, 0, stream>>>(p);
+  }
   return hipGetLastError();
 }
 

@@ -111,7 +111,7 @@ __global__ __launch_bounds__(1024) void stats_kernel(QuantParams p) {
   if (threadIdx.x == 0) {
     float a = 0.0f;
     for (int i = 0; i < kW; ++i) a = fmaxf(a, red[i]);
-    const float ts = p.tscale_unit ? 1.0f : tensor_scale(a);
+    const float ts = (p.tscale_unit || p.mx) ? 1.0f : tensor_scale(a);
     if (is_k) p.k_tscale[b * p.h_kv + h] = ts;
     else p.q_tscale[b * p.h_q + h] = ts;
   }
@@ -140,6 +140,24 @@ __device__ __forceinline__ uint64_t nvfp4_group(const float* xc, float t, uint32
 
 // One workgroup (256 threads) per token: NVFP4 Q rows, NVFP4 K rows and FP8 V
 // into the token's cache slot, then Delta_S for every query head.
+// MXFP4 quantization of one 32-channel block held as 32 centered FP32 values:
+// X = 2^e, e = floor(log2 amax) - 2 clamped to [-127, 127] (-127 for an
+// all-zero block); codes E2M1_RNE_sat(x / X) (exact scaling by a power of two).
+// Returns 16 code bytes (element 2j in the low nibble of byte j).
+__device__ __forceinline__ u32x4 mxfp4_group(const float* xc, uint32_t* scale_code) {
+  float a = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) a = fmaxf(a, __builtin_fabsf(xc[i]));
+  int e = -127;
+  if (a > 0.0f) e = max(-127, min(127, ilog2f(a) - 2));
+  *scale_code = (uint32_t)(e + 127);
+  u32x4 w = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int i = 0; i < 32; ++i)
+    w[i >> 3] |= e2m1_rne_sat(__builtin_ldexpf(xc[i], -e)) << (4 * (i & 7));
+  return w;
+}
+
 __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
   __shared__ float kc[kMaxKvHeadsQuant][kD];
   const int64_t tok = blockIdx.x;
@@ -155,22 +173,42 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
   const int tid = threadIdx.x;
   const int grp_q = p.h_q / p.h_kv;
 
-  // K groups (h_kv * 8 of them) and V
-  for (int i = tid; i < p.h_kv * 8; i += blockDim.x) {
-    const int h = i >> 3, g = i & 7;
-    const uint16_t* src = p.k + (tok * p.h_kv + h) * kD + g * 16;
-    const uint16_t* mean = p.k_mean + ((int64_t)b * p.h_kv + h) * kD + g * 16;
-    float xc[16];
+  // K groups (h_kv * 8 NVFP4 groups or h_kv * 4 MXFP4 blocks) and V
+  if (p.mx) {
+    for (int i = tid; i < p.h_kv * 4; i += blockDim.x) {
+      const int h = i >> 2, g = i & 3;
+      const uint16_t* src = p.k + (tok * p.h_kv + h) * kD + g * 32;
+      const uint16_t* mean = p.k_mean + ((int64_t)b * p.h_kv + h) * kD + g * 32;
+      float xc[32];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      xc[e] = bf16_to_f32(src[e]) - (p.smooth ? bf16_to_f32(mean[e]) : 0.0f);
-      kc[h][g * 16 + e] = xc[e];
+      for (int e = 0; e < 32; ++e) {
+        xc[e] = bf16_to_f32(src[e]) - (p.smooth ? bf16_to_f32(mean[e]) : 0.0f);
+        kc[h][g * 32 + e] = xc[e];
+      }
+      uint32_t sc;
+      const u32x4 w = mxfp4_group(xc, &sc);
+      const int64_t row = (page * p.h_kv + h) * kPage + off;
+      *reinterpret_cast<u32x4*>(p.k_codes + row * 64 + g * 16) = w;
+      p.k_scales[row * 8 + g] = (uint8_t)sc;
+      p.k_scales[row * 8 + 4 + g] = 0;
     }
-    uint32_t sc;
-    const uint64_t w = nvfp4_group(xc, p.k_tscale[b * p.h_kv + h], &sc);
-    const int64_t row = (page * p.h_kv + h) * kPage + off;
-    *reinterpret_cast<uint64_t*>(p.k_codes + row * 64 + g * 8) = w;
-    p.k_scales[row * 8 + g] = (uint8_t)sc;
+  } else {
+    for (int i = tid; i < p.h_kv * 8; i += blockDim.x) {
+      const int h = i >> 3, g = i & 7;
+      const uint16_t* src = p.k + (tok * p.h_kv + h) * kD + g * 16;
+      const uint16_t* mean = p.k_mean + ((int64_t)b * p.h_kv + h) * kD + g * 16;
+      float xc[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        xc[e] = bf16_to_f32(src[e]) - (p.smooth ? bf16_to_f32(mean[e]) : 0.0f);
+        kc[h][g * 16 + e] = xc[e];
+      }
+      uint32_t sc;
+      const uint64_t w = nvfp4_group(xc, p.k_tscale[b * p.h_kv + h], &sc);
+      const int64_t row = (page * p.h_kv + h) * kPage + off;
+      *reinterpret_cast<uint64_t*>(p.k_codes + row * 64 + g * 8) = w;
+      p.k_scales[row * 8 + g] = (uint8_t)sc;
+    }
   }
   for (int i = tid; i < p.h_kv * kD; i += blockDim.x) {
     const int h = i >> 7, c = i & 127;
@@ -178,17 +216,33 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
     p.v_codes[((page * p.h_kv + h) * kD + c) * kPage + off] = (uint8_t)e4m3_rne_sat(v);
   }
   // Q groups
-  for (int i = tid; i < p.h_q * 8; i += blockDim.x) {
-    const int h = i >> 3, g = i & 7;
-    const uint16_t* src = p.q + (tok * p.h_q + h) * kD + g * 16;
-    const uint16_t* mean = p.q_mean + ((int64_t)b * p.h_q + h) * kD + g * 16;
-    float xc[16];
+  if (p.mx) {
+    for (int i = tid; i < p.h_q * 4; i += blockDim.x) {
+      const int h = i >> 2, g = i & 3;
+      const uint16_t* src = p.q + (tok * p.h_q + h) * kD + g * 32;
+      const uint16_t* mean = p.q_mean + ((int64_t)b * p.h_q + h) * kD + g * 32;
+      float xc[32];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) xc[e] = bf16_to_f32(src[e]) - (p.smooth ? bf16_to_f32(mean[e]) : 0.0f);
-    uint32_t sc;
-    const uint64_t w = nvfp4_group(xc, p.q_tscale[b * p.h_q + h], &sc);
-    *reinterpret_cast<uint64_t*>(p.q_codes + (tok * p.h_q + h) * 64 + g * 8) = w;
-    p.q_scales[(tok * p.h_q + h) * 8 + g] = (uint8_t)sc;
+      for (int e = 0; e < 32; ++e) xc[e] = bf16_to_f32(src[e]) - (p.smooth ? bf16_to_f32(mean[e]) : 0.0f);
+      uint32_t sc;
+      const u32x4 w = mxfp4_group(xc, &sc);
+      *reinterpret_cast<u32x4*>(p.q_codes + (tok * p.h_q + h) * 64 + g * 16) = w;
+      p.q_scales[(tok * p.h_q + h) * 8 + g] = (uint8_t)sc;
+      p.q_scales[(tok * p.h_q + h) * 8 + 4 + g] = 0;
+    }
+  } else {
+    for (int i = tid; i < p.h_q * 8; i += blockDim.x) {
+      const int h = i >> 3, g = i & 7;
+      const uint16_t* src = p.q + (tok * p.h_q + h) * kD + g * 16;
+      const uint16_t* mean = p.q_mean + ((int64_t)b * p.h_q + h) * kD + g * 16;
+      float xc[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) xc[e] = bf16_to_f32(src[e]) - (p.smooth ? bf16_to_f32(mean[e]) : 0.0f);
+      uint32_t sc;
+      const uint64_t w = nvfp4_group(xc, p.q_tscale[b * p.h_q + h], &sc);
+      *reinterpret_cast<uint64_t*>(p.q_codes + (tok * p.h_q + h) * 64 + g * 8) = w;
+      p.q_scales[(tok * p.h_q + h) * 8 + g] = (uint8_t)sc;
+    }
   }
   if (!p.smooth) return;
   __syncthreads();

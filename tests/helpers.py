@@ -47,8 +47,9 @@ class Run:
     """One quantize (+ optional prefill) through the HIP path and the oracle."""
 
     def __init__(self, orc, mp, seed, seqlens, h_q, h_kv, outliers=True, smooth=True,
-                 tscale_unit=False, shuffle=True, device="cuda"):
+                 tscale_unit=False, shuffle=True, device="cuda", mxfp4=False):
         self.orc, self.mp = orc, mp
+        self.mxfp4 = mxfp4
         self.seqlens = list(seqlens)
         self.h_q, self.h_kv = h_q, h_kv
         self.smooth = smooth
@@ -62,7 +63,8 @@ class Run:
         slots = np.concatenate([slots_for(self.pt, b, np.arange(n)) for b, n in enumerate(seqlens)]) \
             if cu[-1] > 0 else np.zeros(0, np.int64)
         self.slots = slots
-        flags = (mp.SMOOTH if smooth else 0) | mp.COMPUTE_STATS | (mp.TSCALE_UNIT if tscale_unit else 0)
+        flags = (mp.SMOOTH if smooth else 0) | mp.COMPUTE_STATS | (mp.TSCALE_UNIT if tscale_unit else 0) \
+            | (mp.MXFP4 if mxfp4 else 0)
         self.flags = flags
         # HIP path
         T = int(cu[-1])
@@ -78,7 +80,8 @@ class Run:
         # oracle on the same bits
         self.ref = orc.quantize_qk(bits(q), bits(k), bits(v), cu, slots, max(self.n_pages, 1),
                                    (orc.SMOOTH if smooth else 0) | orc.COMPUTE_STATS |
-                                   (orc.TSCALE_UNIT if tscale_unit else 0))
+                                   (orc.TSCALE_UNIT if tscale_unit else 0) |
+                                   (orc.MXFP4 if mxfp4 else 0))
 
     def gpu_quant(self):
         c = self.cache
@@ -104,7 +107,7 @@ class Run:
         out = torch.full((T, self.h_q, 128), float("nan"), dtype=torch.bfloat16, device="cuda")
         mp.prefill(self.qq, self.cache, self.stats, self.cu_d, dev(q_start), dev(kv_len),
                    dev(self.pt), out, max(self.seqlens),
-                   (mp.SMOOTH if self.smooth else 0) | extra_flags)
+                   (mp.SMOOTH if self.smooth else 0) | (mp.MXFP4 if self.mxfp4 else 0) | extra_flags)
         torch.cuda.synchronize()
         return bits(out)
 
@@ -115,5 +118,5 @@ class Run:
         r = self.ref
         o16, o64 = self.orc.prefill(r["cache"], self.pt, kv_len, r["k_tscale"], r["q_codes"],
                                     r["q_scales"], r["q_tscale"], self.cu, q_start, items,
-                                    smooth=self.smooth)
+                                    smooth=self.smooth, mxfp4=self.mxfp4)
         return o16, o64

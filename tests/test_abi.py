@@ -57,7 +57,7 @@ def _prefill_args(mp, **kw):
 
 @pytest.mark.parametrize("field,value,status", [
     ("head_dim", 64, 2), ("head_dim", 0, 1), ("h_q", 7, 1), ("h_kv", 0, 1), ("batch", 0, 1),
-    ("max_pages", 0, 1), ("flags", 16, 1), ("q_codes", None, 1), ("ds", None, 1),
+    ("max_pages", 0, 1), ("flags", 32, 1), ("q_codes", None, 1), ("ds", None, 1),
     ("max_seqlen_q", -1, 1), ("h_kv", 64, 1),
 ])
 def test_prefill_validation(mp, field, value, status):
@@ -119,7 +119,7 @@ def test_quantize_validation(mp):
     a.ds = None
     assert mp.lib().mpfa_quantize_qk(C.byref(a), None) == 1      # smoothing needs the side cache
     a.ds = 0x1000
-    a.flags = 16
+    a.flags = 32
     assert mp.lib().mpfa_quantize_qk(C.byref(a), None) == 1
     a.flags = 3
     a.head_dim = 96

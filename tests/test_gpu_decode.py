@@ -23,16 +23,17 @@ def mp():
 
 
 class DecodeRun:
-    def __init__(self, orc, mp, seed, kv_lens, h_q, h_kv, smooth=True, outliers=True):
+    def __init__(self, orc, mp, seed, kv_lens, h_q, h_kv, smooth=True, outliers=True, mxfp4=False):
         self.orc, self.mp = orc, mp
         self.kv = np.asarray(kv_lens, np.int32)
         B = len(kv_lens)
         self.B, self.h_q, self.h_kv, self.smooth = B, h_q, h_kv, smooth
+        self.mxfp4 = mxfp4
         ctx = [int(n) - 1 for n in kv_lens]
         self.pt, n_pages = H.make_pages(seed, kv_lens)
         self.n_pages = max(n_pages, 1)
-        flags_s = mp.SMOOTH if smooth else 0
-        oflags_s = orc.SMOOTH if smooth else 0
+        flags_s = (mp.SMOOTH if smooth else 0) | (mp.MXFP4 if mxfp4 else 0)
+        oflags_s = (orc.SMOOTH if smooth else 0) | (orc.MXFP4 if mxfp4 else 0)
         # 1) context cache write with statistics
         q, k, v = H.gen_qkv(seed, ctx, h_q, h_kv, outliers, "cuda")
         cu = np.concatenate([[0], np.cumsum(ctx)]).astype(np.int32)
@@ -67,7 +68,8 @@ class DecodeRun:
                          device="cuda")
         out = torch.full((self.B, self.h_q, 128), float("nan"), dtype=torch.bfloat16, device="cuda")
         mp.decode_paged(self.qq, self.cache, self.stats, self.dev(self.kv), self.dev(self.pt), out,
-                        partition, maxp, ws, mp.SMOOTH if self.smooth else 0)
+                        partition, maxp, ws,
+                        (mp.SMOOTH if self.smooth else 0) | (mp.MXFP4 if self.mxfp4 else 0))
         torch.cuda.synchronize()
         return H.bits(out)
 
@@ -76,7 +78,8 @@ class DecodeRun:
         if items is None:
             items = np.array([(b, h) for b in range(self.B) for h in range(self.h_q)], np.int32)
         o16, _ = self.orc.decode(r["cache"], self.pt, self.kv, r["k_tscale"], r["q_codes"],
-                                 r["q_scales"], r["q_tscale"], partition, items, smooth=self.smooth)
+                                 r["q_scales"], r["q_tscale"], partition, items, smooth=self.smooth,
+                                 mxfp4=self.mxfp4)
         return items, o16
 
 
@@ -137,3 +140,11 @@ def test_decode_matches_prefill_last_row(orc, mp):
     a = H.bf16_f64(H.bits(out)[0])
     b = H.bf16_f64(pre[n - 1])
     assert np.max(np.abs(a - b)) <= 2 ** -7 * np.max(np.abs(b))
+
+
+@pytest.mark.parametrize("smooth", [True, False])
+def test_decode_mxfp4(orc, mp, smooth):
+    """MXFP4 variant: QK on the scaled FP4 MFMA against the oracle's MXFP4 mode."""
+    print(f"case: decode mxfp4 smooth={smooth}", flush=True)
+    run = DecodeRun(orc, mp, 71, [1, 130, 777, 2500], 32, 8, smooth=smooth, mxfp4=True)
+    _cmp(run, 256, f"mxfp4 smooth={smooth}")

@@ -133,3 +133,29 @@ def test_prefill_repeatable_all_modes(orc, mp):
     a = direct.prefill_gpu()
     for _ in range(6):
         assert np.array_equal(direct.prefill_gpu(), a)
+
+
+@pytest.mark.parametrize("smooth", [True, False])
+def test_prefill_mxfp4_ragged(orc, mp, smooth):
+    """MXFP4 variant over a ragged GQA batch, every output row."""
+    print(f"case: mxfp4 prefill smooth={smooth}", flush=True)
+    seqlens = [1, 130, 300, 513]
+    run = H.Run(orc, mp, 19, seqlens, 8, 2, outliers=True, smooth=smooth, mxfp4=True)
+    out = run.prefill_gpu()
+    _check(run, out, _all_items(seqlens, 8), label=f"mxfp4 smooth={smooth}")
+    if smooth:
+        assert np.array_equal(out, run.prefill_gpu(extra_flags=mp.SEED_INIT))
+    for _ in range(4):
+        assert np.array_equal(run.prefill_gpu(), out)
+
+
+def test_prefill_mxfp4_llama_sampled(orc, mp):
+    """MXFP4 variant on the Llama-shaped 16384-token workload, sampled rows."""
+    print("case: mxfp4 llama 16384 sampled", flush=True)
+    n = 16384
+    run = H.Run(orc, mp, 2, [n], 32, 8, outliers=True, mxfp4=True)
+    out = run.prefill_gpu()
+    rng = np.random.default_rng(1)
+    rows = np.unique(np.concatenate([np.arange(0, 200), rng.integers(0, n, 150), [n - 1]]))
+    items = np.array([(0, int(i), h) for i in rows for h in range(0, 32, 5)], np.int32)
+    _check(run, out, items, label="mxfp4 llama sampled")

@@ -123,3 +123,13 @@ def test_append_mode_frozen_stats(orc, mp):
     for key in ("k_codes", "k_scales", "v_codes"):
         assert np.array_equal(getattr(run.cache, key).cpu().numpy(), ref["cache"][key]), key
     assert np.array_equal(H.bits(run.cache.ds), ref["cache"]["ds"])
+
+
+@pytest.mark.parametrize("smooth", [True, False])
+def test_quantize_mxfp4(orc, mp, smooth):
+    """MXFP4 codes, E8M0 scales (bytes 4..7 zero), unit tensor scales and the
+    unchanged means / V / Delta_S, bit for bit."""
+    print(f"case: mxfp4 quantize smooth={smooth}", flush=True)
+    run = H.Run(orc, mp, 13, [1, 200, 333, 64], 8, 2, outliers=True, smooth=smooth, mxfp4=True)
+    _assert_quant_equal(run, smooth=smooth)
+    assert np.all(run.stats.k_tscale.cpu().numpy() == 1.0)
