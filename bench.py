@@ -85,6 +85,8 @@ def parse():
     ap.add_argument("--no-direct", action="store_true", help="skip the unsmoothed prefill variant")
     ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-accuracy", action="store_true",
+                    help="skip the error report against FP64 unquantized attention")
     ap.add_argument("--cpu-rows", type=int, default=16384, help="oracle sample: query rows of head 0")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for memory counters)")
@@ -196,6 +198,44 @@ def decode_bytes(st):
         + wl.batch * 4
 
 
+def fp64_reference(np, st, n_heads, n_rows):
+    """Textbook causal softmax attention in FP64 over the unquantized BF16 inputs
+    (Eq. 2) for a sample: `n_heads` query heads spread over the KV heads and
+    `n_rows` query rows spread over the sequence (first and last included)."""
+    import torch
+    q, k, v = st["q"], st["k"], st["v"]
+    seq, h_q, h_kv = q.shape[0], q.shape[1], k.shape[1]
+    grp = h_q // h_kv
+    heads = sorted({(i * h_q) // n_heads for i in range(n_heads)})
+    rows = np.unique(np.linspace(0, seq - 1, n_rows).astype(np.int64))
+    idx = torch.from_numpy(rows).to(q.device)
+    ref = {}
+    for h in heads:
+        kk = k[:, h // grp].float().cpu().numpy().astype(np.float64)
+        vv = v[:, h // grp].float().cpu().numpy().astype(np.float64)
+        qq = q[idx, h].float().cpu().numpy().astype(np.float64)
+        s = (qq @ kk.T) / math.sqrt(qq.shape[1])
+        s[np.arange(seq)[None, :] > rows[:, None]] = -np.inf
+        pr = np.exp(s - s.max(axis=1, keepdims=True))
+        ref[h] = (pr @ vv) / pr.sum(axis=1, keepdims=True)
+    return {"heads": heads, "rows": rows, "idx": idx, "o": ref}
+
+
+def error_vs_fp64(np, out, ref):
+    """Relative L2 and max-abs error of a BF16 output [T, H, 128] on the sampled
+    rows of `ref`."""
+    rows = ref["idx"].to(out.device)
+    num = den = 0.0
+    mx = 0.0
+    for h in ref["heads"]:
+        o = out[rows, h].float().cpu().numpy().astype(np.float64)
+        d = o - ref["o"][h]
+        num += float((d * d).sum())
+        den += float((ref["o"][h] ** 2).sum())
+        mx = max(mx, float(np.abs(d).max()))
+    return {"rel_l2": math.sqrt(num / den), "max_abs": mx}
+
+
 def cpu_baseline(np, W, st, rows):
     """Time the CPU oracle (as it stands) on a bounded sample of the same prefill
     workload: query head 0, `rows` query rows spread over the sequence."""
@@ -235,6 +275,7 @@ def main():
     mp.lib()
     res = {}
     prefill_ms = quant_ms = decode_ms = 0.0
+    acc = {}
     seq = args.prefill_seq
 
     if not args.no_prefill:
@@ -255,6 +296,14 @@ def main():
         torch.cuda.synchronize()
         quant_ms = sum(t.ms() for t in qt) / args.steps
         prefill_ms = sum(t.ms() for t in pt_) / args.steps
+        acc = {}
+        if not args.no_accuracy:
+            log("FP64 reference attention on sampled rows ...")
+            ref64 = fp64_reference(np, st, 8, 24)
+            acc["sample"] = (f"{len(ref64['rows'])} query rows spread over 0..{seq - 1} x "
+                             f"query heads {ref64['heads']}; FP64 softmax attention of the "
+                             "unquantized BF16 inputs")
+            acc["nvfp4_smoothed"] = error_vs_fp64(np, st["out"], ref64)
         wl = st["wl"]
         pairs = wl.causal_pairs()
         f_qk = 2.0 * 128 * pairs
@@ -299,6 +348,8 @@ def main():
                 ts.append(t2)
             torch.cuda.synchronize()
             direct_ms = sum(t.ms() for t in ts) / args.steps
+            if acc:
+                acc["nvfp4_direct"] = error_vs_fp64(np, std["out"], ref64)
             res["prefill"]["direct_ms"] = direct_ms
             res["prefill"]["rank_one_overhead"] = prefill_ms / direct_ms - 1.0
             del std
@@ -323,12 +374,22 @@ def main():
                 ts.append(t2)
             torch.cuda.synchronize()
             mx_ms = sum(t.ms() for t in ts) / args.steps
+            if acc:
+                acc["mxfp4_smoothed"] = error_vs_fp64(np, sm["out"], ref64)
+                sm["flags"] = mp.MXFP4
+                run_quant(mp, sm)
+                run_prefill(mp, sm)
+                torch.cuda.synchronize()
+                acc["mxfp4_direct"] = error_vs_fp64(np, sm["out"], ref64)
             mx_tf = flops / (mx_ms * 1e-3)
             res["prefill_mxfp4"] = {"ms": mx_ms, "tflops": mx_tf / 1e12,
                                     "frac_fp4_fp8_peak": mx_tf / peak,
                                     "quant_ms": sum(t.ms() for t in qt) / args.steps}
             del sm
             torch.cuda.empty_cache()
+
+    if acc:
+        res["accuracy_vs_fp64"] = acc
 
     if not args.no_decode:
         log(f"setup decode batch {args.decode_batch} ...")
