@@ -113,7 +113,7 @@ typedef enum {
  * by slot_mapping.  Deterministic: identical inputs give identical bytes.
  */
 typedef struct {
-    int32_t batch;            /* sequences in this call (>= 1)                    */
+    int32_t batch;            /* sequences in this call, 1 .. 65535                */
     int32_t total_tokens;     /* T = cu_seqlens[batch] (host copy)               */
     int32_t max_seqlen;       /* host: max tokens of one sequence in this call   */
     int32_t h_q, h_kv;        /* heads; h_q % h_kv == 0, h_q <= MPFA_MAX_HEADS   */

@@ -52,6 +52,7 @@ mpfa_status mpfa_quantize_qk(const mpfa_quant_args* a, mpfa_stream_t stream) {
       !a->v_codes || (smooth && !a->ds))
     return MPFA_ERR_INVALID;
   if ((int64_t)a->batch * (a->h_q + a->h_kv) > INT32_MAX) return MPFA_ERR_INVALID;
+  if (a->batch > 65535) return MPFA_ERR_UNSUPPORTED;   // sequences run on the grid's y dimension
 
   mpfa::QuantParams p{};
   p.batch = a->batch;
@@ -63,6 +64,8 @@ mpfa_status mpfa_quantize_qk(const mpfa_quant_args* a, mpfa_stream_t stream) {
   p.stats_k = p.compute_stats;
   p.tscale_unit = (a->flags & MPFA_TSCALE_UNIT) != 0;
   p.mx = (a->flags & MPFA_MXFP4) != 0;
+  p.max_seqlen = a->max_seqlen;
+  p.need_partials = (p.compute_stats && p.smooth) || !(p.tscale_unit || p.mx);
   p.cu_seqlens = a->cu_seqlens;
   p.q = static_cast<const uint16_t*>(a->q);
   p.k = static_cast<const uint16_t*>(a->k);

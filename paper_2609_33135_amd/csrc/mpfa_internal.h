@@ -10,8 +10,9 @@ namespace mpfa {
 constexpr int kMaxKvHeadsQuant = 32;
 
 struct QuantParams {
-  int batch, total_tokens, h_q, h_kv;
+  int batch, total_tokens, max_seqlen, h_q, h_kv;
   int smooth, compute_stats, stats_k, tscale_unit;
+  int need_partials;  // per-token statistics needed: means (STATS + SMOOTH) or amax (NVFP4 t)
   int mx;           // Q/K in MXFP4 (E8M0 per 32 channels, tensor scale 1)
   const int32_t* cu_seqlens;
   const uint16_t* q;

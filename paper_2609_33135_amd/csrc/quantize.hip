@@ -10,111 +10,187 @@
 
 namespace mpfa {
 
-// One workgroup per (sequence, head), 16 waves.  Each wave sums one 128-token
-// block at a time (lane l owns channels 2l, 2l+1; loads issued 16 tokens
-// ahead), FP32 in token order; wave 0 then adds the block partials in block
-// order, divides in FP32 and rounds to BF16.  A second pass takes the amax of
-// the centered values for the power-of-two tensor scale.
-__global__ __launch_bounds__(1024) void stats_kernel(QuantParams p) {
-  constexpr int kW = 16;                     // waves per workgroup
-  __shared__ float part[kW][kD];
-  __shared__ float meanf[kD];
-  __shared__ float red[kW];
-  const int Htot = p.stats_k ? p.h_q + p.h_kv : p.h_q;
-  const int b = blockIdx.x / Htot;
-  const int hh = blockIdx.x % Htot;
-  const bool is_k = hh >= p.h_q;
-  const int h = is_k ? hh - p.h_q : hh;
-  const int H = is_k ? p.h_kv : p.h_q;
-  const uint32_t* x = reinterpret_cast<const uint32_t*>(is_k ? p.k : p.q);   // BF16 pairs
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int c0 = 2 * lane;
-  const int64_t t0 = p.cu_seqlens[b];
-  const int n = p.cu_seqlens[b + 1] - p.cu_seqlens[b];
-  uint16_t* mean_out = (is_k ? p.k_mean : p.q_mean) + ((int64_t)b * H + h) * kD;
-  // BF16 pair of token t (relative to the sequence) for this lane's channels
-  auto row = [&](int t) { return x[((t0 + t) * H + h) * (kD / 2) + lane]; };
+// ---------------------------------------------------------------------------
+// Sequence statistics (Eq. 7) and tensor scales.
+//
+// stats_partial_kernel: one workgroup per (sequence, 128-token block).  Lane
+// groups of 16 own one head row (8 channels per lane, 16-byte loads); each lane
+// sums its channels over the block's tokens in token order (FP32) and keeps
+// their max and min.  The amax of the centered values needs no second read:
+// x -> fl(x - mean) is monotone, so max_t |fl(x_t - mean)| is reached at the
+// channel's max or min.  A one-block sequence is finished in place; otherwise
+// the block partials (sum, max, min) are parked in the q_codes rows of the
+// sequence, which quantize_kernel overwrites later on the same stream.
+// stats_final_kernel adds the block partials in block order and finishes.
+// ---------------------------------------------------------------------------
+constexpr int kStatUnits = 4;   // (head, 8-channel) units per thread and pass
 
-  if (p.compute_stats) {
-    float tot0 = 0.0f, tot1 = 0.0f;
-    if (p.smooth && n > 0) {
-      const int nblk = (n + 127) / 128;
-      for (int blk0 = 0; blk0 < nblk; blk0 += kW) {
-        const int blk = blk0 + wv;
-        float s0 = 0.0f, s1 = 0.0f;
-        if (blk < nblk) {
-          const int tb = blk * 128, te = min(n, tb + 128);
-          for (int t = tb; t < te; t += 16) {
-            uint32_t v[16];
+struct StatsShape {
+  int hs;                 // heads with statistics: h_q, plus h_kv with stats_k
+  bool want_sum, want_amax;
+};
+
+__device__ __forceinline__ StatsShape stats_shape(const QuantParams& p) {
+  StatsShape s;
+  s.hs = p.h_q + (p.stats_k ? p.h_kv : 0);
+  s.want_sum = p.compute_stats && p.smooth;
+  s.want_amax = !(p.tscale_unit || p.mx);
+  return s;
+}
+
+// block partials of block blk: float [3][hs][128] (sum, max, min).  Block i <
+// nblk-1 uses the q_codes rows of its own 128 tokens; the last block uses the
+// rows of block nblk-2 after that block's partials (2 * 1536 * hs bytes fit in
+// the 8192 * h_q bytes of 128 token rows since hs <= 2 h_q).
+__device__ __forceinline__ float* partial_ptr(const QuantParams& p, int64_t t0, int nblk, int blk, int hs) {
+  const bool last = blk == nblk - 1;
+  const int64_t r = last ? nblk - 2 : blk;
+  uint8_t* base = p.q_codes + (t0 + r * 128) * (int64_t)p.h_q * 64;
+  if (last) base += (int64_t)3 * hs * kD * 4;
+  return reinterpret_cast<float*>(base);
+}
+
+// mean of head hh (0..h_q-1: Q, then K) and its BF16 output row
+__device__ __forceinline__ uint16_t* mean_row(const QuantParams& p, int b, int hh) {
+  return hh < p.h_q ? p.q_mean + ((int64_t)b * p.h_q + hh) * kD
+                    : p.k_mean + ((int64_t)b * p.h_kv + (hh - p.h_q)) * kD;
+}
+
+__device__ __forceinline__ void write_tscale(const QuantParams& p, int b, int hh, float amax) {
+  const float ts = (p.tscale_unit || p.mx) ? 1.0f : tensor_scale(amax);
+  if (hh < p.h_q) p.q_tscale[b * p.h_q + hh] = ts;
+  else p.k_tscale[b * p.h_kv + (hh - p.h_q)] = ts;
+}
+
+__global__ __launch_bounds__(256) void stats_partial_kernel(QuantParams p) {
+  const int b = blockIdx.y, blk = blockIdx.x;
+  const int64_t t0 = p.cu_seqlens[b];
+  const int n = p.cu_seqlens[b + 1] - (int)t0;
+  const int nblk = (n + 127) >> 7;
+  if (blk >= nblk) return;
+  const StatsShape ss = stats_shape(p);
+  const int tb = blk * 128, te = min(n, tb + 128);
+  const int nunits = ss.hs * 16;
+  for (int u0 = 0; u0 < nunits; u0 += 256 * kStatUnits) {
+    const uint4* src[kStatUnits];
+    int64_t stride[kStatUnits];   // in 16-byte words per token
+    bool act[kStatUnits];
+    float sm[kStatUnits][8], mx[kStatUnits][8], mn[kStatUnits][8];
 #pragma unroll
-            for (int u = 0; u < 16; ++u) v[u] = (t + u < te) ? row(t + u) : 0u;
+    for (int k = 0; k < kStatUnits; ++k) {
+      const int u = u0 + k * 256 + threadIdx.x;
+      act[k] = u < nunits;
+      const int hh = act[k] ? u >> 4 : 0, oct = u & 15;
+      const bool isq = hh < p.h_q;
+      const int H = isq ? p.h_q : p.h_kv;
+      const int h = isq ? hh : hh - p.h_q;
+      const uint16_t* base = isq ? p.q : p.k;
+      src[k] = reinterpret_cast<const uint4*>(base + ((t0 + tb) * H + h) * kD + oct * 8);
+      stride[k] = (int64_t)H * (kD / 8);
 #pragma unroll
-            for (int u = 0; u < 16; ++u) {
-              if (t + u < te) {
-                s0 += __uint_as_float(v[u] << 16);
-                s1 += __uint_as_float(v[u] & 0xFFFF0000u);
-              }
+      for (int e = 0; e < 8; ++e) {
+        sm[k][e] = 0.0f;
+        mx[k][e] = -INFINITY;
+        mn[k][e] = INFINITY;
+      }
+    }
+    for (int t = tb; t < te; t += 4) {
+      uint4 w[4][kStatUnits];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int k = 0; k < kStatUnits; ++k)
+          w[j][k] = (act[k] && t + j < te) ? src[k][(int64_t)(t - tb + j) * stride[k]] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (t + j < te) {
+#pragma unroll
+          for (int k = 0; k < kStatUnits; ++k) {
+            const uint32_t wd[4] = {w[j][k].x, w[j][k].y, w[j][k].z, w[j][k].w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float x = __uint_as_float((e & 1) ? (wd[e >> 1] & 0xFFFF0000u) : (wd[e >> 1] << 16));
+              sm[k][e] += x;
+              mx[k][e] = fmaxf(mx[k][e], x);
+              mn[k][e] = fminf(mn[k][e], x);
             }
           }
         }
-        part[wv][c0] = s0;
-        part[wv][c0 + 1] = s1;
-        __syncthreads();
-        if (wv == 0) {
-          for (int j = 0; j < kW && blk0 + j < nblk; ++j) {
-            tot0 += part[j][c0];
-            tot1 += part[j][c0 + 1];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kStatUnits; ++k) {
+      const int u = u0 + k * 256 + threadIdx.x;
+      const int hh = u >> 4, oct = u & 15;
+      if (nblk == 1) {
+        // one block: its partial sum is the total (0 + partial, exact)
+        float amax = 0.0f;
+        if (act[k]) {
+          uint16_t* mrow = mean_row(p, b, hh) + oct * 8;
+          float mu[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            uint16_t m = 0;
+            if (ss.want_sum) m = bf16_rne(__fdiv_rn(sm[k][e], (float)n));
+            else if (!p.compute_stats && p.smooth) m = mrow[e];
+            if (p.compute_stats) mrow[e] = m;
+            mu[e] = bf16_to_f32(m);
           }
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            amax = fmaxf(amax, fmaxf(__builtin_fabsf(mx[k][e] - mu[e]), __builtin_fabsf(mn[k][e] - mu[e])));
         }
-        __syncthreads();
+        // 16 lanes of one head row (units of one head are 16 consecutive lanes)
+        for (int off = 1; off < 16; off <<= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
+        if (act[k] && oct == 0) write_tscale(p, b, hh, amax);
+      } else if (act[k]) {
+        float* part = partial_ptr(p, t0, nblk, blk, ss.hs) + hh * kD + oct * 8;
+#pragma unroll
+        for (int e = 0; e < 8; e += 4) {
+          *reinterpret_cast<float4*>(part + e) = make_float4(sm[k][e], sm[k][e + 1], sm[k][e + 2], sm[k][e + 3]);
+          *reinterpret_cast<float4*>(part + ss.hs * kD + e) =
+              make_float4(mx[k][e], mx[k][e + 1], mx[k][e + 2], mx[k][e + 3]);
+          *reinterpret_cast<float4*>(part + 2 * ss.hs * kD + e) =
+              make_float4(mn[k][e], mn[k][e + 1], mn[k][e + 2], mn[k][e + 3]);
+        }
       }
     }
-    if (wv == 0) {
-      uint16_t m0 = 0, m1 = 0;
-      if (p.smooth && n > 0) {
-        m0 = bf16_rne(__fdiv_rn(tot0, (float)n));
-        m1 = bf16_rne(__fdiv_rn(tot1, (float)n));
-      }
-      mean_out[c0] = m0;
-      mean_out[c0 + 1] = m1;
-      meanf[c0] = bf16_to_f32(m0);
-      meanf[c0 + 1] = bf16_to_f32(m1);
-    }
-  } else if (wv == 0) {
-    meanf[c0] = p.smooth ? bf16_to_f32(mean_out[c0]) : 0.0f;
-    meanf[c0 + 1] = p.smooth ? bf16_to_f32(mean_out[c0 + 1]) : 0.0f;
   }
-  __syncthreads();
+}
 
-  // amax of the centered values (any order)
-  float amax = 0.0f;
-  const float m0 = meanf[c0], m1 = meanf[c0 + 1];
-  int t = wv;
-  for (; t + 3 * kW < n; t += 4 * kW) {
-    uint32_t v[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = row(t + u * kW);
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      amax = fmaxf(amax, __builtin_fabsf(__uint_as_float(v[u] << 16) - m0));
-      amax = fmaxf(amax, __builtin_fabsf(__uint_as_float(v[u] & 0xFFFF0000u) - m1));
+// One workgroup of 128 threads (one per channel) per (head, sequence): block
+// partials added in block order, FP32 divide, BF16 rounding; tensor scale from
+// the per-channel max / min.  Also covers sequences with no tokens and the
+// calls that need no per-token statistics at all (need_partials == 0).
+__global__ __launch_bounds__(128) void stats_final_kernel(QuantParams p) {
+  __shared__ float red[2];
+  const int hh = blockIdx.x, b = blockIdx.y, c = threadIdx.x;
+  const int64_t t0 = p.cu_seqlens[b];
+  const int n = p.cu_seqlens[b + 1] - (int)t0;
+  const int nblk = (n + 127) >> 7;
+  if (p.need_partials && nblk == 1) return;   // finished by stats_partial_kernel
+  const StatsShape ss = stats_shape(p);
+  float tot = 0.0f, mx = -INFINITY, mn = INFINITY;
+  const bool have = p.need_partials && nblk >= 2;
+  if (have) {
+    for (int blk = 0; blk < nblk; ++blk) {
+      const float* part = partial_ptr(p, t0, nblk, blk, ss.hs) + hh * kD + c;
+      tot += part[0];
+      mx = fmaxf(mx, part[ss.hs * kD]);
+      mn = fminf(mn, part[2 * ss.hs * kD]);
     }
   }
-  for (; t < n; t += kW) {
-    const uint32_t v = row(t);
-    amax = fmaxf(amax, __builtin_fabsf(__uint_as_float(v << 16) - m0));
-    amax = fmaxf(amax, __builtin_fabsf(__uint_as_float(v & 0xFFFF0000u) - m1));
-  }
+  uint16_t* mrow = mean_row(p, b, hh);
+  uint16_t m = 0;
+  if (ss.want_sum && n > 0) m = bf16_rne(__fdiv_rn(tot, (float)n));
+  else if (!p.compute_stats && p.smooth) m = mrow[c];
+  if (p.compute_stats) mrow[c] = m;
+  const float mu = bf16_to_f32(m);
+  float amax = have ? fmaxf(__builtin_fabsf(mx - mu), __builtin_fabsf(mn - mu)) : 0.0f;
   for (int off = 32; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
-  if (lane == 0) red[wv] = amax;
+  if ((c & 63) == 0) red[c >> 6] = amax;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    float a = 0.0f;
-    for (int i = 0; i < kW; ++i) a = fmaxf(a, red[i]);
-    const float ts = (p.tscale_unit || p.mx) ? 1.0f : tensor_scale(a);
-    if (is_k) p.k_tscale[b * p.h_kv + h] = ts;
-    else p.q_tscale[b * p.h_q + h] = ts;
-  }
+  if (c == 0) write_tscale(p, b, hh, fmaxf(red[0], red[1]));
 }
 
 // NVFP4 quantization of one 16-channel group held as 16 centered FP32 values:
@@ -138,8 +214,6 @@ __device__ __forceinline__ uint64_t nvfp4_group(const float* xc, float t, uint32
   return w;
 }
 
-// One workgroup (256 threads) per token: NVFP4 Q rows, NVFP4 K rows and FP8 V
-// into the token's cache slot, then Delta_S for every query head.
 // MXFP4 quantization of one 32-channel block held as 32 centered FP32 values:
 // X = 2^e, e = floor(log2 amax) - 2 clamped to [-127, 127] (-127 for an
 // all-zero block); codes E2M1_RNE_sat(x / X) (exact scaling by a power of two).
@@ -158,101 +232,158 @@ __device__ __forceinline__ u32x4 mxfp4_group(const float* xc, uint32_t* scale_co
   return w;
 }
 
-__global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
-  __shared__ float kc[kMaxKvHeadsQuant][kD];
-  const int64_t tok = blockIdx.x;
-  // sequence of this token: binary search over cu_seqlens
-  int lo = 0, hi = p.batch - 1;
-  while (lo < hi) {
-    int mid = (lo + hi + 1) >> 1;
-    if (p.cu_seqlens[mid] <= tok) lo = mid; else hi = mid - 1;
-  }
-  const int b = lo;
-  const int64_t slot = p.slot_mapping[tok];
-  const int64_t page = slot / kPage, off = slot % kPage;
-  const int tid = threadIdx.x;
-  const int grp_q = p.h_q / p.h_kv;
+// ---------------------------------------------------------------------------
+// Quantization and cache write.  One workgroup (256 threads) per (sequence,
+// 64-token chunk).  Group u of the chunk's Q rows is at u * group_elems in the
+// packed input, so consecutive lanes read and write consecutive groups.  V:
+// when the chunk's 64 tokens fill one cache page in order (the common prefill
+// case), each lane converts two channels of all 64 tokens and writes their two
+// channel-major 64-byte page rows whole; otherwise one byte per (token,
+// channel).  Delta_S: one lane per (token, query head), K_c recomputed from the
+// BF16 row (the FP32 subtraction is exact and deterministic).
+// ---------------------------------------------------------------------------
+constexpr int kChunk = 64;
 
-  // K groups (h_kv * 8 NVFP4 groups or h_kv * 4 MXFP4 blocks) and V
-  if (p.mx) {
-    for (int i = tid; i < p.h_kv * 4; i += blockDim.x) {
-      const int h = i >> 2, g = i & 3;
-      const uint16_t* src = p.k + (tok * p.h_kv + h) * kD + g * 32;
-      const uint16_t* mean = p.k_mean + ((int64_t)b * p.h_kv + h) * kD + g * 32;
-      float xc[32];
+template <bool MX>
+__device__ __forceinline__ void quant_rows(const QuantParams& p, const uint16_t* x, const uint16_t* mean_base,
+                                           const float* tscale, int H, int64_t tok0, int cnt, bool to_cache,
+                                           uint8_t* codes_out, uint8_t* scales_out) {
+  constexpr int G = MX ? 4 : 8;          // groups per row
+  constexpr int E = MX ? 32 : 16;        // elements per group
+  const int ngr = cnt * H * G;
+  for (int u = threadIdx.x; u < ngr; u += blockDim.x) {
+    const int g = u % G, ih = u / G;
+    const int h = ih % H, i = ih / H;
+    const uint4* src = reinterpret_cast<const uint4*>(x + (tok0 * H) * kD) + (int64_t)u * (E / 8);
+    const uint4* mrow = reinterpret_cast<const uint4*>(mean_base + (int64_t)h * kD + g * E);
+    float xc[E];
 #pragma unroll
-      for (int e = 0; e < 32; ++e) {
-        xc[e] = bf16_to_f32(src[e]) - (p.smooth ? bf16_to_f32(mean[e]) : 0.0f);
-        kc[h][g * 32 + e] = xc[e];
+    for (int w = 0; w < E / 8; ++w) {
+      const uint4 v = src[w];
+      const uint4 m = p.smooth ? mrow[w] : make_uint4(0, 0, 0, 0);
+      const uint32_t vv[4] = {v.x, v.y, v.z, v.w}, mm[4] = {m.x, m.y, m.z, m.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t sh = (e & 1) ? 0u : 16u;
+        const float xv = __uint_as_float(sh ? (vv[e >> 1] << 16) : (vv[e >> 1] & 0xFFFF0000u));
+        const float mv = __uint_as_float(sh ? (mm[e >> 1] << 16) : (mm[e >> 1] & 0xFFFF0000u));
+        xc[w * 8 + e] = xv - mv;
       }
-      uint32_t sc;
-      const u32x4 w = mxfp4_group(xc, &sc);
-      const int64_t row = (page * p.h_kv + h) * kPage + off;
-      *reinterpret_cast<u32x4*>(p.k_codes + row * 64 + g * 16) = w;
-      p.k_scales[row * 8 + g] = (uint8_t)sc;
-      p.k_scales[row * 8 + 4 + g] = 0;
     }
-  } else {
-    for (int i = tid; i < p.h_kv * 8; i += blockDim.x) {
-      const int h = i >> 3, g = i & 7;
-      const uint16_t* src = p.k + (tok * p.h_kv + h) * kD + g * 16;
-      const uint16_t* mean = p.k_mean + ((int64_t)b * p.h_kv + h) * kD + g * 16;
-      float xc[16];
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        xc[e] = bf16_to_f32(src[e]) - (p.smooth ? bf16_to_f32(mean[e]) : 0.0f);
-        kc[h][g * 16 + e] = xc[e];
-      }
-      uint32_t sc;
-      const uint64_t w = nvfp4_group(xc, p.k_tscale[b * p.h_kv + h], &sc);
-      const int64_t row = (page * p.h_kv + h) * kPage + off;
-      *reinterpret_cast<uint64_t*>(p.k_codes + row * 64 + g * 8) = w;
-      p.k_scales[row * 8 + g] = (uint8_t)sc;
+    int64_t row;   // destination row: token row of q_codes, or cache row
+    if (to_cache) {
+      const int64_t slot = p.slot_mapping[tok0 + i];
+      row = ((slot / kPage) * p.h_kv + h) * kPage + slot % kPage;
+    } else {
+      row = (tok0 + i) * H + h;
+    }
+    uint32_t sc;
+    if (MX) {
+      const u32x4 w = mxfp4_group(xc, &sc);
+      *reinterpret_cast<u32x4*>(codes_out + row * 64 + g * 16) = w;
+      scales_out[row * 8 + g] = (uint8_t)sc;
+      scales_out[row * 8 + 4 + g] = 0;
+    } else {
+      const uint64_t w = nvfp4_group(xc, tscale[h], &sc);
+      *reinterpret_cast<uint64_t*>(codes_out + row * 64 + g * 8) = w;
+      scales_out[row * 8 + g] = (uint8_t)sc;
     }
   }
-  for (int i = tid; i < p.h_kv * kD; i += blockDim.x) {
-    const int h = i >> 7, c = i & 127;
-    const float v = bf16_to_f32(p.v[(tok * p.h_kv + h) * kD + c]);
-    p.v_codes[((page * p.h_kv + h) * kD + c) * kPage + off] = (uint8_t)e4m3_rne_sat(v);
+}
+
+template <bool MX>
+__global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
+  __shared__ int page_run;   // 1: the chunk's 64 tokens are slots 0..63 of one page, in order
+  const int b = blockIdx.y;
+  const int64_t t0 = p.cu_seqlens[b];
+  const int n = p.cu_seqlens[b + 1] - (int)t0;
+  const int i0 = blockIdx.x * kChunk;
+  if (i0 >= n) return;
+  const int cnt = min(kChunk, n - i0);
+  const int64_t tok0 = t0 + i0;
+  const int tid = threadIdx.x;
+
+  if (tid < 64) {
+    bool ok = cnt == kChunk;
+    if (ok) {
+      const int64_t s0 = p.slot_mapping[tok0];
+      ok = (s0 % kPage == 0) && p.slot_mapping[tok0 + tid] == s0 + tid;
+    }
+    const bool all = __builtin_amdgcn_ballot_w64(!ok) == 0;
+    if (tid == 0) page_run = all ? 1 : 0;
   }
-  // Q groups
-  if (p.mx) {
-    for (int i = tid; i < p.h_q * 4; i += blockDim.x) {
-      const int h = i >> 2, g = i & 3;
-      const uint16_t* src = p.q + (tok * p.h_q + h) * kD + g * 32;
-      const uint16_t* mean = p.q_mean + ((int64_t)b * p.h_q + h) * kD + g * 32;
-      float xc[32];
+
+  // Q rows (packed output) and K rows (cache)
+  quant_rows<MX>(p, p.q, p.q_mean + (int64_t)b * p.h_q * kD, p.q_tscale + b * p.h_q, p.h_q, tok0, cnt,
+                 false, p.q_codes, p.q_scales);
+  quant_rows<MX>(p, p.k, p.k_mean + (int64_t)b * p.h_kv * kD, p.k_tscale + b * p.h_kv, p.h_kv, tok0, cnt,
+                 true, p.k_codes, p.k_scales);
+  __syncthreads();
+
+  // V -> E4M3, channel-major page rows
+  if (page_run) {
+    const int64_t page = p.slot_mapping[tok0] / kPage;
+    for (int u = tid; u < p.h_kv * (kD / 2); u += blockDim.x) {
+      const int h = u / (kD / 2), cp = u % (kD / 2);
+      const uint32_t* src = reinterpret_cast<const uint32_t*>(p.v + (tok0 * p.h_kv + h) * kD) + cp;
+      const int64_t tstride = (int64_t)p.h_kv * (kD / 2);
+      uint8_t* dst = p.v_codes + ((page * p.h_kv + h) * kD + 2 * cp) * kPage;
+      // 16 tokens at a time: 16 bytes of each of the two channel rows
+      for (int qq = 0; qq < kPage; qq += 16) {
+        uint32_t w[16];
 #pragma unroll
-      for (int e = 0; e < 32; ++e) xc[e] = bf16_to_f32(src[e]) - (p.smooth ? bf16_to_f32(mean[e]) : 0.0f);
-      uint32_t sc;
-      const u32x4 w = mxfp4_group(xc, &sc);
-      *reinterpret_cast<u32x4*>(p.q_codes + (tok * p.h_q + h) * 64 + g * 16) = w;
-      p.q_scales[(tok * p.h_q + h) * 8 + g] = (uint8_t)sc;
-      p.q_scales[(tok * p.h_q + h) * 8 + 4 + g] = 0;
+        for (int j = 0; j < 16; ++j) w[j] = src[(int64_t)(qq + j) * tstride];
+        u32x4 r0, r1;   // bytes of channels 2cp and 2cp+1
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint32_t a = 0, c = 0;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            a |= e4m3_rne_sat(__uint_as_float(w[4 * q + j] << 16)) << (8 * j);
+            c |= e4m3_rne_sat(__uint_as_float(w[4 * q + j] & 0xFFFF0000u)) << (8 * j);
+          }
+          r0[q] = a;
+          r1[q] = c;
+        }
+        *reinterpret_cast<u32x4*>(dst + qq) = r0;
+        *reinterpret_cast<u32x4*>(dst + kPage + qq) = r1;
+      }
     }
   } else {
-    for (int i = tid; i < p.h_q * 8; i += blockDim.x) {
-      const int h = i >> 3, g = i & 7;
-      const uint16_t* src = p.q + (tok * p.h_q + h) * kD + g * 16;
-      const uint16_t* mean = p.q_mean + ((int64_t)b * p.h_q + h) * kD + g * 16;
-      float xc[16];
-#pragma unroll
-      for (int e = 0; e < 16; ++e) xc[e] = bf16_to_f32(src[e]) - (p.smooth ? bf16_to_f32(mean[e]) : 0.0f);
-      uint32_t sc;
-      const uint64_t w = nvfp4_group(xc, p.q_tscale[b * p.h_q + h], &sc);
-      *reinterpret_cast<uint64_t*>(p.q_codes + (tok * p.h_q + h) * 64 + g * 8) = w;
-      p.q_scales[(tok * p.h_q + h) * 8 + g] = (uint8_t)sc;
+    for (int u = tid; u < cnt * p.h_kv * kD; u += blockDim.x) {
+      const int c = u % kD, ih = u / kD;
+      const int h = ih % p.h_kv, i = ih / p.h_kv;
+      const int64_t slot = p.slot_mapping[tok0 + i];
+      const float v = bf16_to_f32(p.v[(tok0 + i) * p.h_kv * kD + (int64_t)h * kD + c]);
+      p.v_codes[(((slot / kPage) * p.h_kv + h) * kD + c) * kPage + slot % kPage] = (uint8_t)e4m3_rne_sat(v);
     }
   }
   if (!p.smooth) return;
-  __syncthreads();
-  // Delta_S[h_q] = BF16(fma chain over channels of Qbar[h_q] * K_c[h_kv])
-  for (int h = tid; h < p.h_q; h += blockDim.x) {
-    const uint16_t* qm = p.q_mean + ((int64_t)b * p.h_q + h) * kD;
-    const float* k = kc[h / grp_q];
+
+  // Delta_S[h] = BF16(sum_c Qbar[h][c] * K_c[c]) as an FMA chain over c from +0
+  const int grp = p.h_q / p.h_kv;
+  for (int u = tid; u < cnt * p.h_q; u += blockDim.x) {
+    const int h = u % p.h_q, i = u / p.h_q, hk = h / grp;
+    const uint4* kr = reinterpret_cast<const uint4*>(p.k + ((tok0 + i) * p.h_kv + hk) * kD);
+    const uint4* km = reinterpret_cast<const uint4*>(p.k_mean + ((int64_t)b * p.h_kv + hk) * kD);
+    const uint4* qm = reinterpret_cast<const uint4*>(p.q_mean + ((int64_t)b * p.h_q + h) * kD);
     float d = 0.0f;
-    for (int c = 0; c < kD; ++c) d = __builtin_fmaf(bf16_to_f32(qm[c]), k[c], d);
-    p.ds[(page * p.h_q + h) * kPage + off] = bf16_rne(d);
+#pragma unroll 4
+    for (int w = 0; w < kD / 8; ++w) {
+      const uint4 kv = kr[w], mv = km[w], qv = qm[w];
+      const uint32_t k4[4] = {kv.x, kv.y, kv.z, kv.w}, m4[4] = {mv.x, mv.y, mv.z, mv.w},
+                     q4[4] = {qv.x, qv.y, qv.z, qv.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const bool lo = (e & 1) == 0;
+        const float kx = __uint_as_float(lo ? (k4[e >> 1] << 16) : (k4[e >> 1] & 0xFFFF0000u));
+        const float mx = __uint_as_float(lo ? (m4[e >> 1] << 16) : (m4[e >> 1] & 0xFFFF0000u));
+        const float qx = __uint_as_float(lo ? (q4[e >> 1] << 16) : (q4[e >> 1] & 0xFFFF0000u));
+        d = __builtin_fmaf(qx, kx - mx, d);
+      }
+    }
+    const int64_t slot = p.slot_mapping[tok0 + i];
+    p.ds[((slot / kPage) * p.h_q + h) * kPage + slot % kPage] = bf16_rne(d);
   }
 }
 
@@ -263,12 +394,19 @@ __global__ void convert_kernel(int fmt, const float* x, int64_t n, uint8_t* out)
 }
 
 hipError_t launch_quantize(const QuantParams& p, hipStream_t stream) {
-  const int Htot = p.stats_k ? p.h_q + p.h_kv : p.h_q;
-  stats_kernel<<<dim3(p.batch * Htot), dim3(1024), 0, stream>>>(p);
+  const int hs = p.h_q + (p.stats_k ? p.h_kv : 0);
+  if (p.need_partials && p.max_seqlen > 0) {
+    stats_partial_kernel<<<dim3((p.max_seqlen + 127) / 128, p.batch), dim3(256), 0, stream>>>(p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  stats_final_kernel<<<dim3(hs, p.batch), dim3(128), 0, stream>>>(p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (p.total_tokens > 0) {
-    quantize_kernel<<<dim3(p.total_tokens), dim3(256), 0, stream>>>(p);
+  if (p.total_tokens > 0 && p.max_seqlen > 0) {
+    const dim3 grid((p.max_seqlen + kChunk - 1) / kChunk, p.batch);
+    if (p.mx) quantize_kernel<true><<<grid, dim3(256), 0, stream>>>(p);
+    else quantize_kernel<false><<<grid, dim3(256), 0, stream>>>(p);
     e = hipGetLastError();
   }
   return e;

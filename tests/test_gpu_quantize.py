@@ -133,3 +133,52 @@ def test_quantize_mxfp4(orc, mp, smooth):
     run = H.Run(orc, mp, 13, [1, 200, 333, 64], 8, 2, outliers=True, smooth=smooth, mxfp4=True)
     _assert_quant_equal(run, smooth=smooth)
     assert np.all(run.stats.k_tscale.cpu().numpy() == 1.0)
+
+
+def _append_call(orc, mp, run, pos, seed, mx):
+    """A later call on sequence 0 of `run` with frozen statistics: tokens at
+    positions `pos`, quantized by the HIP path and the oracle from the same
+    cache state; compares every output bit."""
+    n = len(pos)
+    q, k, v = H.gen_qkv(seed, [n], run.h_q, run.h_kv, True, "cuda")
+    slots = H.slots_for(run.pt, 0, pos)
+    cu = np.array([0, n], np.int32)
+    qq = mp.QuantQ(n, 1, run.h_q, "cuda")
+    fmt = mp.MXFP4 if mx else 0
+    mp.quantize_qk(q, k, v, torch.from_numpy(cu).cuda(), torch.from_numpy(slots).cuda(),
+                   run.cache, run.stats, qq, mp.SMOOTH | fmt, n)
+    torch.cuda.synchronize()
+    r = run.ref
+    ref = orc.quantize_qk(H.bits(q), H.bits(k), H.bits(v), cu, slots, run.n_pages,
+                          orc.SMOOTH | (orc.MXFP4 if mx else 0), q_mean=r["q_mean"],
+                          k_mean=r["k_mean"], k_tscale=r["k_tscale"], cache=r["cache"])
+    assert np.array_equal(qq.codes.cpu().numpy(), ref["q_codes"])
+    assert np.array_equal(qq.scales.cpu().numpy(), ref["q_scales"])
+    assert np.array_equal(qq.tscale.cpu().numpy(), ref["q_tscale"])
+    for key in ("k_codes", "k_scales", "v_codes"):
+        assert np.array_equal(getattr(run.cache, key).cpu().numpy(), ref["cache"][key]), key
+    assert np.array_equal(H.bits(run.cache.ds), ref["cache"]["ds"])
+    # the HIP path's cache now equals the oracle's: later calls continue from it
+    r["cache"] = ref["cache"]
+
+
+@pytest.mark.parametrize("mx", [False, True])
+def test_chunked_calls_frozen_stats(orc, mp, mx):
+    """Chunked prefill: a first 700-token call computes the statistics, then
+    300-token chunks with frozen statistics start on a page boundary (whole
+    pages written by one chunk) and mid-page (byte-wise page writes); the
+    Q tensor scale of each chunk comes from its own tokens over several
+    128-token blocks."""
+    print(f"case: chunked calls mx={mx}", flush=True)
+    run = H.Run(orc, mp, 17, [1400], 8, 2, outliers=True, mxfp4=mx)
+    # overwrite positions 704..1003 (page aligned) and 1037..1336 (mid page)
+    _append_call(orc, mp, run, np.arange(704, 1004), 71, mx)
+    _append_call(orc, mp, run, np.arange(1037, 1337), 72, mx)
+
+
+def test_quantize_empty_and_short_sequences(orc, mp):
+    """Sequences with 0 tokens (means 0, tensor scale 1), one short block, and a
+    last block of a single token after a full one."""
+    print("case: ragged batch [0, 5, 129, 0, 256]", flush=True)
+    run = H.Run(orc, mp, 19, [0, 5, 129, 0, 256], 4, 2, outliers=True)
+    _assert_quant_equal(run)
