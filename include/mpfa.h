@@ -231,10 +231,13 @@ mpfa_status mpfa_decode_paged(const mpfa_decode_args* args, void* workspace, siz
 /* ------------------------------------------------------------------------ */
 /* Utilities                                                                  */
 /* ------------------------------------------------------------------------ */
-/* Element-wise device conversion used by the quantizer, exposed so that its
- * rounding can be checked exhaustively: fmt 0 = FP32 -> E4M3 (RNE, saturating
- * at 448, sign kept), fmt 1 = FP32 -> E2M1 (RNE, saturating at 6, sign kept,
- * one code per output byte).  x and out are device pointers of n elements. */
+/* Element-wise device conversions, exposed so that their rounding can be
+ * checked exhaustively: fmt 0 = FP32 -> E4M3 (RNE, saturating at 448, sign
+ * kept), fmt 1 = FP32 -> E2M1 (RNE, saturating at 6, sign kept, one code per
+ * output byte), both written out from the format definitions; fmt 2 and 3 =
+ * the same two conversions through the gfx950 hardware converters, as the
+ * quantization pass uses them (must give identical bytes).  x and out are
+ * device pointers of n elements; MPFA_ERR_INVALID for another fmt. */
 mpfa_status mpfa_convert(int32_t fmt, const float* x, int64_t n, uint8_t* out,
                          mpfa_stream_t stream);
 

@@ -205,5 +205,7 @@ def decode_paged(qq: QuantQ, cache: PagedCache, stats: SeqStats, kv_len, page_ta
 
 
 def convert(fmt: int, x, out, stream=None):
-    """mpfa_convert: fmt 0 FP32 -> E4M3, fmt 1 FP32 -> E2M1 (one code per byte)."""
+    """mpfa_convert: fmt 0 FP32 -> E4M3, fmt 1 FP32 -> E2M1 (one code per byte),
+    written from the format definitions; fmt 2 / 3 the same through the hardware
+    converters the quantization pass uses."""
     _check(lib().mpfa_convert(fmt, _ptr(x), x.numel(), _ptr(out), _stream(stream)), "mpfa_convert")

@@ -199,7 +199,7 @@ mpfa_status mpfa_decode_paged(const mpfa_decode_args* a, void* workspace, size_t
 }
 
 mpfa_status mpfa_convert(int32_t fmt, const float* x, int64_t n, uint8_t* out, mpfa_stream_t stream) {
-  if ((fmt != 0 && fmt != 1) || n < 0 || (n > 0 && (!x || !out))) return MPFA_ERR_INVALID;
+  if (fmt < 0 || fmt > 3 || n < 0 || (n > 0 && (!x || !out))) return MPFA_ERR_INVALID;
   if (n > (int64_t)UINT32_MAX * 256) return MPFA_ERR_INVALID;
   return mpfa::launch_convert(fmt, x, n, out, reinterpret_cast<hipStream_t>(stream)) == hipSuccess
              ? MPFA_OK

@@ -173,11 +173,28 @@ __global__ __launch_bounds__(128) void stats_final_kernel(QuantParams p) {
   float tot = 0.0f, mx = -INFINITY, mn = INFINITY;
   const bool have = p.need_partials && nblk >= 2;
   if (have) {
-    for (int blk = 0; blk < nblk; ++blk) {
-      const float* part = partial_ptr(p, t0, nblk, blk, ss.hs) + hh * kD + c;
-      tot += part[0];
-      mx = fmaxf(mx, part[ss.hs * kD]);
-      mn = fminf(mn, part[2 * ss.hs * kD]);
+    // partials of 32 blocks in flight, added in block order
+    constexpr int kAhead = 32;
+    for (int blk0 = 0; blk0 < nblk; blk0 += kAhead) {
+      float ps[kAhead], px[kAhead], pn[kAhead];
+#pragma unroll
+      for (int j = 0; j < kAhead; ++j) {
+        ps[j] = 0.0f;
+        px[j] = -INFINITY;
+        pn[j] = INFINITY;
+        if (blk0 + j < nblk) {
+          const float* part = partial_ptr(p, t0, nblk, blk0 + j, ss.hs) + hh * kD + c;
+          ps[j] = part[0];
+          px[j] = part[ss.hs * kD];
+          pn[j] = part[2 * ss.hs * kD];
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kAhead; ++j) {
+        if (blk0 + j < nblk) tot += ps[j];
+        mx = fmaxf(mx, px[j]);
+        mn = fminf(mn, pn[j]);
+      }
     }
   }
   uint16_t* mrow = mean_row(p, b, hh);
@@ -193,6 +210,39 @@ __global__ __launch_bounds__(128) void stats_final_kernel(QuantParams p) {
   if (c == 0) write_tscale(p, b, hh, fmaxf(red[0], red[1]));
 }
 
+// Element conversions through the gfx950 converters.  Over every finite FP32
+// input these give the same bytes as e2m1_rne_sat / e4m3_rne_sat (checked
+// exhaustively on the device): v_cvt_scalef32_pk_fp4_f32 rounds to nearest
+// even and saturates at 6 after dividing by the power of two in its scale
+// operand; v_cvt_pk_fp8_f32 rounds to nearest even, and clamping to +-448
+// first makes it saturate as the E4M3 encoder does.
+__device__ __forceinline__ uint32_t fp4_pair(uint32_t w, float a, float b, float pow2, int sel) {
+  switch (sel) {   // the byte selector must be an immediate
+    case 0: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 0);
+    case 1: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 1);
+    case 2: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 2);
+    default: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 3);
+  }
+}
+__device__ __forceinline__ uint32_t fp8_sat_pair(uint32_t w, float a, float b, bool hi) {
+  a = fminf(fmaxf(a, -448.0f), 448.0f);
+  b = fminf(fmaxf(b, -448.0f), 448.0f);
+  return hi ? (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)w, true)
+            : (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)w, false);
+}
+
+// RN(x / s) from r = RN(1 / s): one product and one residual correction.  For
+// divisors s = 2^k * (E4M3 value) this equals the correctly rounded quotient
+// for every FP32 x whose quotient is at least 2^-100 in magnitude (checked
+// exhaustively on the device over all x and all 126 positive E4M3 values);
+// smaller quotients round to the zero E2M1 code either way.  The sign is
+// restored for x = -0 (the correction would return +0).
+__device__ __forceinline__ float div_by_scale(float x, float s, float r) {
+  const float q0 = x * r;
+  const float e = __builtin_fmaf(-s, q0, x);
+  return __builtin_copysignf(__builtin_fmaf(e, r, q0), x);
+}
+
 // NVFP4 quantization of one 16-channel group held as 16 centered FP32 values:
 // returns 8 code bytes (as a 64-bit word, low nibble first) and the scale byte.
 __device__ __forceinline__ uint64_t nvfp4_group(const float* xc, float t, uint32_t* scale_code) {
@@ -202,22 +252,32 @@ __device__ __forceinline__ uint64_t nvfp4_group(const float* xc, float t, uint32
   const uint32_t s = e4m3_rne_sat(__fdiv_rn(a, 6.0f * t));
   *scale_code = s;
   const float sd = e4m3_value(s);
-  uint64_t w = 0;
+  uint32_t w0 = 0, w1 = 0;
   if (sd == 0.0f) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) w |= (uint64_t)((__float_as_uint(xc[i]) >> 28) & 8u) << (4 * i);
+    for (int i = 0; i < 8; ++i) {
+      w0 |= ((__float_as_uint(xc[i]) >> 28) & 8u) << (4 * i);
+      w1 |= ((__float_as_uint(xc[8 + i]) >> 28) & 8u) << (4 * i);
+    }
   } else {
     const float scale = t * sd;   // exact: t is a power of two
+    const float r = __fdiv_rn(1.0f, scale);
+    float y[16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) w |= (uint64_t)e2m1_rne_sat(__fdiv_rn(xc[i], scale)) << (4 * i);
+    for (int i = 0; i < 16; ++i) y[i] = div_by_scale(xc[i], scale, r);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      w0 = fp4_pair(w0, y[2 * j], y[2 * j + 1], 1.0f, j);
+      w1 = fp4_pair(w1, y[8 + 2 * j], y[8 + 2 * j + 1], 1.0f, j);
+    }
   }
-  return w;
+  return (uint64_t)w0 | ((uint64_t)w1 << 32);
 }
 
 // MXFP4 quantization of one 32-channel block held as 32 centered FP32 values:
 // X = 2^e, e = floor(log2 amax) - 2 clamped to [-127, 127] (-127 for an
-// all-zero block); codes E2M1_RNE_sat(x / X) (exact scaling by a power of two).
-// Returns 16 code bytes (element 2j in the low nibble of byte j).
+// all-zero block); codes E2M1_RNE_sat(x / X).  Returns 16 code bytes (element
+// 2j in the low nibble of byte j).
 __device__ __forceinline__ u32x4 mxfp4_group(const float* xc, uint32_t* scale_code) {
   float a = 0.0f;
 #pragma unroll
@@ -225,10 +285,14 @@ __device__ __forceinline__ u32x4 mxfp4_group(const float* xc, uint32_t* scale_co
   int e = -127;
   if (a > 0.0f) e = max(-127, min(127, ilog2f(a) - 2));
   *scale_code = (uint32_t)(e + 127);
+  // e = -127 only for an all-zero block, whose codes keep just the signs under
+  // any scale; 2^-126 keeps the scale operand a normal number
+  const float pw = __builtin_ldexpf(1.0f, max(e, -126));
   u32x4 w = {0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int i = 0; i < 32; ++i)
-    w[i >> 3] |= e2m1_rne_sat(__builtin_ldexpf(xc[i], -e)) << (4 * (i & 7));
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) w[q] = fp4_pair(w[q], xc[8 * q + 2 * j], xc[8 * q + 2 * j + 1], pw, j);
   return w;
 }
 
@@ -336,12 +400,11 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
         u32x4 r0, r1;   // bytes of channels 2cp and 2cp+1
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          uint32_t a = 0, c = 0;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            a |= e4m3_rne_sat(__uint_as_float(w[4 * q + j] << 16)) << (8 * j);
-            c |= e4m3_rne_sat(__uint_as_float(w[4 * q + j] & 0xFFFF0000u)) << (8 * j);
-          }
+          const uint32_t* wq = w + 4 * q;
+          uint32_t a = fp8_sat_pair(0u, __uint_as_float(wq[0] << 16), __uint_as_float(wq[1] << 16), false);
+          a = fp8_sat_pair(a, __uint_as_float(wq[2] << 16), __uint_as_float(wq[3] << 16), true);
+          uint32_t c = fp8_sat_pair(0u, __uint_as_float(wq[0] & 0xFFFF0000u), __uint_as_float(wq[1] & 0xFFFF0000u), false);
+          c = fp8_sat_pair(c, __uint_as_float(wq[2] & 0xFFFF0000u), __uint_as_float(wq[3] & 0xFFFF0000u), true);
           r0[q] = a;
           r1[q] = c;
         }
@@ -390,7 +453,14 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
 __global__ void convert_kernel(int fmt, const float* x, int64_t n, uint8_t* out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
-  out[i] = (uint8_t)(fmt == 0 ? e4m3_rne_sat(x[i]) : e2m1_rne_sat(x[i]));
+  uint32_t c;
+  switch (fmt) {
+    case 0: c = e4m3_rne_sat(x[i]); break;
+    case 1: c = e2m1_rne_sat(x[i]); break;
+    case 2: c = fp8_sat_pair(0u, x[i], 0.0f, false) & 0xFFu; break;
+    default: c = fp4_pair(0u, x[i], 0.0f, 1.0f, 0) & 0xFu; break;
+  }
+  out[i] = (uint8_t)c;
 }
 
 hipError_t launch_quantize(const QuantParams& p, hipStream_t stream) {

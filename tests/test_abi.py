@@ -130,5 +130,6 @@ def test_quantize_validation(mp):
 
 
 def test_convert_validation(mp):
-    assert mp.lib().mpfa_convert(2, None, 0, None, None) == 1
+    assert mp.lib().mpfa_convert(4, None, 0, None, None) == 1
+    assert mp.lib().mpfa_convert(-1, None, 0, None, None) == 1
     assert mp.lib().mpfa_convert(0, None, 5, None, None) == 1

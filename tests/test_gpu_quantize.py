@@ -74,8 +74,9 @@ def test_quantize_llama_prefill_shape(orc, mp):
 
 
 def test_convert_sweep(orc, mp):
-    """Device E4M3 / E2M1 encoders against the oracle's over a stride of all FP32
-    bit patterns plus dense neighbourhoods of every rounding boundary."""
+    """Device E4M3 / E2M1 encoders (software and the hardware converters the
+    quantization pass uses) against the oracle's over a stride of all FP32 bit
+    patterns plus dense neighbourhoods of every rounding boundary."""
     print("case: codec sweep", flush=True)
     pats = np.arange(0, 1 << 32, 61, dtype=np.uint64).astype(np.uint32)
     x = pats.view(np.float32)
@@ -88,7 +89,8 @@ def test_convert_sweep(orc, mp):
         extra += [r, r | np.uint32(0x80000000)]
     x = np.concatenate([x, np.concatenate(extra).view(np.float32)])
     xd = torch.from_numpy(x).cuda()
-    for fmt, ref_fn in ((0, orc.e4m3_encode), (1, orc.e2m1_encode)):
+    for fmt, ref_fn in ((0, orc.e4m3_encode), (1, orc.e2m1_encode), (2, orc.e4m3_encode),
+                        (3, orc.e2m1_encode)):
         out = torch.empty(x.size, dtype=torch.uint8, device="cuda")
         mp.convert(fmt, xd, out)
         torch.cuda.synchronize()
