@@ -245,11 +245,19 @@ __device__ __forceinline__ float div_by_scale(float x, float s, float r) {
 
 // NVFP4 quantization of one 16-channel group held as 16 centered FP32 values:
 // returns 8 code bytes (as a 64-bit word, low nibble first) and the scale byte.
-__device__ __forceinline__ uint64_t nvfp4_group(const float* xc, float t, uint32_t* scale_code) {
+// rcp_sd[c] = RN(1 / e4m3_value(c)) for the positive E4M3 codes; with a
+// power-of-two t, RN(1 / (t * sd)) = rcp_sd / t and RN(1 / (6 t)) = RN(1/6) / t.
+constexpr float kRcp6 = 0x1.555556p-3f;   // RN(1/6)
+
+__device__ __forceinline__ uint64_t nvfp4_group(const float* xc, float t, const float* rcp_sd,
+                                                uint32_t* scale_code) {
   float a = 0.0f;
 #pragma unroll
   for (int i = 0; i < 16; ++i) a = fmaxf(a, __builtin_fabsf(xc[i]));
-  const uint32_t s = e4m3_rne_sat(__fdiv_rn(a, 6.0f * t));
+  const int kt = ilog2f(t);
+  float q = div_by_scale(a, 6.0f * t, __builtin_ldexpf(kRcp6, -kt));   // RN(amax / (6 t))
+  if (!(q < 0x1p100f)) q = 0x1p100f;   // an overflowing quotient saturates like +inf would
+  const uint32_t s = fp8_sat_pair(0u, q, 0.0f, false) & 0xFFu;         // E4M3_RNE_sat
   *scale_code = s;
   const float sd = e4m3_value(s);
   uint32_t w0 = 0, w1 = 0;
@@ -261,14 +269,24 @@ __device__ __forceinline__ uint64_t nvfp4_group(const float* xc, float t, uint32
     }
   } else {
     const float scale = t * sd;   // exact: t is a power of two
-    const float r = __fdiv_rn(1.0f, scale);
-    float y[16];
+    const float r = __builtin_ldexpf(rcp_sd[s], -kt);
+    if (a * r < 0x1p100f) {
+      float y[16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) y[i] = div_by_scale(xc[i], scale, r);
+      for (int i = 0; i < 16; ++i) y[i] = div_by_scale(xc[i], scale, r);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      w0 = fp4_pair(w0, y[2 * j], y[2 * j + 1], 1.0f, j);
-      w1 = fp4_pair(w1, y[8 + 2 * j], y[8 + 2 * j + 1], 1.0f, j);
+      for (int j = 0; j < 4; ++j) {
+        w0 = fp4_pair(w0, y[2 * j], y[2 * j + 1], 1.0f, j);
+        w1 = fp4_pair(w1, y[8 + 2 * j], y[8 + 2 * j + 1], 1.0f, j);
+      }
+    } else {
+      // quotients near the FP32 range (a frozen K tensor scale far below a
+      // later token): IEEE division, saturating encoder
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        w0 |= e2m1_rne_sat(__fdiv_rn(xc[i], scale)) << (4 * i);
+        w1 |= e2m1_rne_sat(__fdiv_rn(xc[8 + i], scale)) << (4 * i);
+      }
     }
   }
   return (uint64_t)w0 | ((uint64_t)w1 << 32);
@@ -307,19 +325,23 @@ __device__ __forceinline__ u32x4 mxfp4_group(const float* xc, uint32_t* scale_co
 // BF16 row (the FP32 subtraction is exact and deterministic).
 // ---------------------------------------------------------------------------
 constexpr int kChunk = 64;
+constexpr int kMeanStride = kD * 2 + 16;   // bytes per BF16 mean row in LDS (padded: rows on distinct banks)
 
 template <bool MX>
-__device__ __forceinline__ void quant_rows(const QuantParams& p, const uint16_t* x, const uint16_t* mean_base,
+__device__ __forceinline__ void quant_rows(const QuantParams& p, const uint16_t* x, const uint8_t* mean_base,
                                            const float* tscale, int H, int64_t tok0, int cnt, bool to_cache,
-                                           uint8_t* codes_out, uint8_t* scales_out) {
+                                           uint8_t* codes_out, uint8_t* scales_out, const float* rcp_sd) {
   constexpr int G = MX ? 4 : 8;          // groups per row
   constexpr int E = MX ? 32 : 16;        // elements per group
+  constexpr int kStep = 256 / G;         // rows advanced per loop step (blockDim 256)
   const int ngr = cnt * H * G;
-  for (int u = threadIdx.x; u < ngr; u += blockDim.x) {
-    const int g = u % G, ih = u / G;
-    const int h = ih % H, i = ih / H;
+  // group u = (i * H + h) * G + g, tracked incrementally over u += 256
+  const int g = threadIdx.x % G;
+  int h = (threadIdx.x / G) % H, i = (threadIdx.x / G) / H;
+  const int di = kStep / H, dh = kStep % H;
+  for (int u = threadIdx.x; u < ngr; u += 256) {
     const uint4* src = reinterpret_cast<const uint4*>(x + (tok0 * H) * kD) + (int64_t)u * (E / 8);
-    const uint4* mrow = reinterpret_cast<const uint4*>(mean_base + (int64_t)h * kD + g * E);
+    const uint4* mrow = reinterpret_cast<const uint4*>(mean_base + h * kMeanStride + g * E * 2);
     float xc[E];
 #pragma unroll
     for (int w = 0; w < E / 8; ++w) {
@@ -328,9 +350,9 @@ __device__ __forceinline__ void quant_rows(const QuantParams& p, const uint16_t*
       const uint32_t vv[4] = {v.x, v.y, v.z, v.w}, mm[4] = {m.x, m.y, m.z, m.w};
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const uint32_t sh = (e & 1) ? 0u : 16u;
-        const float xv = __uint_as_float(sh ? (vv[e >> 1] << 16) : (vv[e >> 1] & 0xFFFF0000u));
-        const float mv = __uint_as_float(sh ? (mm[e >> 1] << 16) : (mm[e >> 1] & 0xFFFF0000u));
+        const bool lo = (e & 1) == 0;
+        const float xv = __uint_as_float(lo ? (vv[e >> 1] << 16) : (vv[e >> 1] & 0xFFFF0000u));
+        const float mv = __uint_as_float(lo ? (mm[e >> 1] << 16) : (mm[e >> 1] & 0xFFFF0000u));
         xc[w * 8 + e] = xv - mv;
       }
     }
@@ -348,9 +370,15 @@ __device__ __forceinline__ void quant_rows(const QuantParams& p, const uint16_t*
       scales_out[row * 8 + g] = (uint8_t)sc;
       scales_out[row * 8 + 4 + g] = 0;
     } else {
-      const uint64_t w = nvfp4_group(xc, tscale[h], &sc);
+      const uint64_t w = nvfp4_group(xc, tscale[h], rcp_sd, &sc);
       *reinterpret_cast<uint64_t*>(codes_out + row * 64 + g * 8) = w;
       scales_out[row * 8 + g] = (uint8_t)sc;
+    }
+    i += di;
+    h += dh;
+    if (h >= H) {
+      h -= H;
+      ++i;
     }
   }
 }
@@ -358,6 +386,8 @@ __device__ __forceinline__ void quant_rows(const QuantParams& p, const uint16_t*
 template <bool MX>
 __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
   __shared__ int page_run;   // 1: the chunk's 64 tokens are slots 0..63 of one page, in order
+  __shared__ float rcp_sd[128];
+  extern __shared__ __attribute__((aligned(16))) uint8_t sm_mean[];   // [h_q + h_kv][kMeanStride]
   const int b = blockIdx.y;
   const int64_t t0 = p.cu_seqlens[b];
   const int n = p.cu_seqlens[b + 1] - (int)t0;
@@ -376,12 +406,27 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
     const bool all = __builtin_amdgcn_ballot_w64(!ok) == 0;
     if (tid == 0) page_run = all ? 1 : 0;
   }
+  if (!MX && tid < 128) rcp_sd[tid] = (tid & 0x7F) && tid < 0x7F ? __fdiv_rn(1.0f, e4m3_value(tid)) : 0.0f;
+  // the sequence's Q and K means (zero rows without smoothing)
+  for (int u = tid; u < (p.h_q + p.h_kv) * (kD / 8); u += blockDim.x) {
+    const int hh = u / (kD / 8), w = u % (kD / 8);
+    uint4 m = make_uint4(0, 0, 0, 0);
+    if (p.smooth) {
+      const uint16_t* row = hh < p.h_q ? p.q_mean + ((int64_t)b * p.h_q + hh) * kD
+                                       : p.k_mean + ((int64_t)b * p.h_kv + (hh - p.h_q)) * kD;
+      m = reinterpret_cast<const uint4*>(row)[w];
+    }
+    *reinterpret_cast<uint4*>(sm_mean + hh * kMeanStride + w * 16) = m;
+  }
+  __syncthreads();
+  const uint8_t* qmean_s = sm_mean;
+  const uint8_t* kmean_s = sm_mean + p.h_q * kMeanStride;
 
   // Q rows (packed output) and K rows (cache)
-  quant_rows<MX>(p, p.q, p.q_mean + (int64_t)b * p.h_q * kD, p.q_tscale + b * p.h_q, p.h_q, tok0, cnt,
-                 false, p.q_codes, p.q_scales);
-  quant_rows<MX>(p, p.k, p.k_mean + (int64_t)b * p.h_kv * kD, p.k_tscale + b * p.h_kv, p.h_kv, tok0, cnt,
-                 true, p.k_codes, p.k_scales);
+  quant_rows<MX>(p, p.q, qmean_s, p.q_tscale + b * p.h_q, p.h_q, tok0, cnt,
+                 false, p.q_codes, p.q_scales, rcp_sd);
+  quant_rows<MX>(p, p.k, kmean_s, p.k_tscale + b * p.h_kv, p.h_kv, tok0, cnt,
+                 true, p.k_codes, p.k_scales, rcp_sd);
   __syncthreads();
 
   // V -> E4M3, channel-major page rows
@@ -423,30 +468,57 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
   }
   if (!p.smooth) return;
 
-  // Delta_S[h] = BF16(sum_c Qbar[h][c] * K_c[c]) as an FMA chain over c from +0
+  // Delta_S[h] = BF16(sum_c Qbar[h][c] * K_c[c]) as an FMA chain over c from +0.
+  // One lane per (token, KV head): K_c is formed once and feeds the chains of
+  // up to 8 query heads of the group at a time.
   const int grp = p.h_q / p.h_kv;
-  for (int u = tid; u < cnt * p.h_q; u += blockDim.x) {
-    const int h = u % p.h_q, i = u / p.h_q, hk = h / grp;
+  for (int u = tid; u < cnt * p.h_kv; u += blockDim.x) {
+    const int hk = u % p.h_kv, i = u / p.h_kv;
     const uint4* kr = reinterpret_cast<const uint4*>(p.k + ((tok0 + i) * p.h_kv + hk) * kD);
-    const uint4* km = reinterpret_cast<const uint4*>(p.k_mean + ((int64_t)b * p.h_kv + hk) * kD);
-    const uint4* qm = reinterpret_cast<const uint4*>(p.q_mean + ((int64_t)b * p.h_q + h) * kD);
-    float d = 0.0f;
-#pragma unroll 4
-    for (int w = 0; w < kD / 8; ++w) {
-      const uint4 kv = kr[w], mv = km[w], qv = qm[w];
-      const uint32_t k4[4] = {kv.x, kv.y, kv.z, kv.w}, m4[4] = {mv.x, mv.y, mv.z, mv.w},
-                     q4[4] = {qv.x, qv.y, qv.z, qv.w};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const bool lo = (e & 1) == 0;
-        const float kx = __uint_as_float(lo ? (k4[e >> 1] << 16) : (k4[e >> 1] & 0xFFFF0000u));
-        const float mx = __uint_as_float(lo ? (m4[e >> 1] << 16) : (m4[e >> 1] & 0xFFFF0000u));
-        const float qx = __uint_as_float(lo ? (q4[e >> 1] << 16) : (q4[e >> 1] & 0xFFFF0000u));
-        d = __builtin_fmaf(qx, kx - mx, d);
-      }
-    }
+    const uint4* km = reinterpret_cast<const uint4*>(kmean_s + hk * kMeanStride);
     const int64_t slot = p.slot_mapping[tok0 + i];
-    p.ds[((slot / kPage) * p.h_q + h) * kPage + slot % kPage] = bf16_rne(d);
+    uint16_t* dsrow = p.ds + ((slot / kPage) * p.h_q + hk * grp) * kPage + slot % kPage;
+    for (int j0 = 0; j0 < grp; j0 += 8) {
+      const int nj = min(8, grp - j0);
+      const uint8_t* qm = qmean_s + (hk * grp + j0) * kMeanStride;
+      float d[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) d[j] = 0.0f;
+      for (int half = 0; half < 2; ++half) {
+        // one 128-byte line of the K row per burst: a row read piecewise over a
+        // long loop gets evicted from L2 between its pieces
+        uint4 kh[8];
+#pragma unroll
+        for (int w = 0; w < 8; ++w) kh[w] = kr[half * 8 + w];
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+          const uint4 kv = kh[w], mv = km[half * 8 + w];
+          const uint32_t k4[4] = {kv.x, kv.y, kv.z, kv.w}, m4[4] = {mv.x, mv.y, mv.z, mv.w};
+          float kc[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const bool lo = (e & 1) == 0;
+            kc[e] = __uint_as_float(lo ? (k4[e >> 1] << 16) : (k4[e >> 1] & 0xFFFF0000u)) -
+                    __uint_as_float(lo ? (m4[e >> 1] << 16) : (m4[e >> 1] & 0xFFFF0000u));
+          }
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            if (j < nj) {
+              const uint4 qv = *reinterpret_cast<const uint4*>(qm + j * kMeanStride + (half * 8 + w) * 16);
+              const uint32_t q4[4] = {qv.x, qv.y, qv.z, qv.w};
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const float qx = __uint_as_float((e & 1) == 0 ? (q4[e >> 1] << 16) : (q4[e >> 1] & 0xFFFF0000u));
+                d[j] = __builtin_fmaf(qx, kc[e], d[j]);
+              }
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (j < nj) dsrow[(int64_t)(j0 + j) * kPage] = bf16_rne(d[j]);
+    }
   }
 }
 
@@ -475,8 +547,9 @@ hipError_t launch_quantize(const QuantParams& p, hipStream_t stream) {
   if (e != hipSuccess) return e;
   if (p.total_tokens > 0 && p.max_seqlen > 0) {
     const dim3 grid((p.max_seqlen + kChunk - 1) / kChunk, p.batch);
-    if (p.mx) quantize_kernel<true><<<grid, dim3(256), 0, stream>>>(p);
-    else quantize_kernel<false><<<grid, dim3(256), 0, stream>>>(p);
+    const size_t lds = (size_t)(p.h_q + p.h_kv) * kMeanStride;
+    if (p.mx) quantize_kernel<true><<<grid, dim3(256), lds, stream>>>(p);
+    else quantize_kernel<false><<<grid, dim3(256), lds, stream>>>(p);
     e = hipGetLastError();
   }
   return e;
