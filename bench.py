@@ -236,6 +236,16 @@ def error_vs_fp64(np, out, ref):
     return {"rel_l2": math.sqrt(num / den), "max_abs": mx}
 
 
+def quant_bytes(wl, seq):
+    """Algorithmic HBM bytes of one quantization / cache-write pass: the
+    statistics read Q and K, the quantizer reads Q, K, V and writes the NVFP4 /
+    MXFP4 rows (64 code + 8 scale bytes), the FP8 V bytes and Delta_S."""
+    row = 128 * 2
+    reads = seq * (2 * (wl.h_q + wl.h_kv) * row + wl.h_kv * row)
+    writes = seq * (wl.h_q * 72 + wl.h_kv * 72 + wl.h_kv * 128 + wl.h_q * 2)
+    return reads + writes
+
+
 def cpu_baseline(np, W, st, rows):
     """Time the CPU oracle (as it stands) on a bounded sample of the same prefill
     workload: query head 0, `rows` query rows spread over the sequence."""
@@ -312,8 +322,13 @@ def main():
         achieved = flops / (prefill_ms * 1e-3)
         roof_t = f_qk / PEAK_FP4 + f_pv / PEAK_FP8
         peak = flops / roof_t
+        qb = quant_bytes(wl, seq)
         res["prefill"] = {"ms": prefill_ms, "tflops": achieved / 1e12, "quant_ms": quant_ms,
+                          "layer_ms": quant_ms + prefill_ms,
                           "causal_pairs": pairs, "flop": flops}
+        res["quant"] = {"ms": quant_ms, "bytes": qb, "GB/s": qb / (quant_ms * 1e-3) / 1e9,
+                        "frac_hbm": qb / (quant_ms * 1e-3) / PEAK_HBM,
+                        "kernels": "stats_partial_kernel + stats_final_kernel + quantize_kernel"}
         res["roofline"] = {"bound": "mfma", "achieved": achieved / 1e12, "peak": peak / 1e12,
                            "unit": "TFLOP/s", "frac": achieved / peak,
                            "traffic": measured_traffic("prefill_kernel"),
@@ -340,14 +355,19 @@ def main():
             for _ in range(args.warmup):
                 run_quant(mp, std)
                 run_prefill(mp, std)
-            ts = []
+            ts, tq = [], []
             for _ in range(args.steps):
-                run_quant(mp, std)
+                with Timer(torch) as t1:
+                    run_quant(mp, std)
                 with Timer(torch) as t2:
                     run_prefill(mp, std)
+                tq.append(t1)
                 ts.append(t2)
             torch.cuda.synchronize()
             direct_ms = sum(t.ms() for t in ts) / args.steps
+            dq_ms = sum(t.ms() for t in tq) / args.steps
+            res["prefill"]["direct_quant_ms"] = dq_ms
+            res["prefill"]["direct_layer_ms"] = dq_ms + direct_ms
             if acc:
                 acc["nvfp4_direct"] = error_vs_fp64(np, std["out"], ref64)
             res["prefill"]["direct_ms"] = direct_ms
@@ -382,9 +402,10 @@ def main():
                 torch.cuda.synchronize()
                 acc["mxfp4_direct"] = error_vs_fp64(np, sm["out"], ref64)
             mx_tf = flops / (mx_ms * 1e-3)
+            mq_ms = sum(t.ms() for t in qt) / args.steps
             res["prefill_mxfp4"] = {"ms": mx_ms, "tflops": mx_tf / 1e12,
                                     "frac_fp4_fp8_peak": mx_tf / peak,
-                                    "quant_ms": sum(t.ms() for t in qt) / args.steps}
+                                    "quant_ms": mq_ms, "layer_ms": mq_ms + mx_ms}
             del sm
             torch.cuda.empty_cache()
 
