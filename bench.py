@@ -348,6 +348,17 @@ def main():
                 ts.append(t2)
             torch.cuda.synchronize()
             res["prefill"]["seed_init_ms"] = sum(t.ms() for t in ts) / args.steps
+            log("prefill with the compensation added element-wise (placement comparison) ...")
+            st["flags"] = mp.SMOOTH | mp.SEED_ELEMWISE
+            for _ in range(args.warmup):
+                run_prefill(mp, st)
+            ts = []
+            for _ in range(args.steps):
+                with Timer(torch) as t2:
+                    run_prefill(mp, st)
+                ts.append(t2)
+            torch.cuda.synchronize()
+            res["prefill"]["seed_elementwise_ms"] = sum(t.ms() for t in ts) / args.steps
             st["flags"] = mp.SMOOTH
             log("prefill direct (unsmoothed) variant ...")
             del st["cache"]
@@ -372,6 +383,8 @@ def main():
                 acc["nvfp4_direct"] = error_vs_fp64(np, std["out"], ref64)
             res["prefill"]["direct_ms"] = direct_ms
             res["prefill"]["rank_one_overhead"] = prefill_ms / direct_ms - 1.0
+            res["prefill"]["seed_init_overhead"] = res["prefill"]["seed_init_ms"] / direct_ms - 1.0
+            res["prefill"]["elementwise_overhead"] = res["prefill"]["seed_elementwise_ms"] / direct_ms - 1.0
             del std
         if not args.no_cpu_baseline:
             res["cpu_baseline"] = cpu_baseline(np, W, st, args.cpu_rows)

@@ -79,6 +79,12 @@ typedef enum {
 #define MPFA_SEED_INIT     8u  /* prefill: load the rank-one term 1 Delta_S^T as the input
                                   accumulator of the first QK MFMA instead of issuing the
                                   BF16 rank-one MFMA; results are bit-identical            */
+#define MPFA_SEED_ELEMWISE 32u /* prefill: the placement the rank-one seed replaces (Sec. 3.2,
+                                  Sec. 7.4 Fig. 10), kept for comparison: the QK accumulator
+                                  starts at zero and Delta_S is added to every score in FP32
+                                  after the product, before masking.  Agrees with the seeded
+                                  placements up to FP32 rounding order (not bit-identical).
+                                  Exclusive with MPFA_SEED_INIT.                          */
 #define MPFA_MXFP4        16u  /* Q/K in MXFP4 instead of NVFP4 (quantize, prefill, decode):
                                   one E8M0 scale per 32 channels (scale bytes 0..3 of the
                                   8-byte scale row; bytes 4..7 zero), tensor scales 1, and
@@ -161,7 +167,7 @@ typedef struct {
     int32_t batch, h_q, h_kv, head_dim;
     int32_t max_seqlen_q;     /* host: max query tokens of one sequence          */
     int32_t max_pages;        /* page_table row length                           */
-    uint32_t flags;           /* MPFA_SMOOTH, MPFA_SEED_INIT, MPFA_MXFP4         */
+    uint32_t flags;           /* MPFA_SMOOTH, MPFA_SEED_INIT or MPFA_SEED_ELEMWISE, MPFA_MXFP4 */
     const int32_t* cu_seqlens_q; /* [batch+1] query tokens                       */
     const int32_t* q_start;   /* [batch] absolute position of query 0            */
     const int32_t* kv_len;    /* [batch] keys in the cache (>= q_start + n_q)    */

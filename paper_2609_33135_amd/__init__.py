@@ -13,7 +13,7 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libmpfa.so")
 
 MPFA_OK, MPFA_ERR_INVALID, MPFA_ERR_UNSUPPORTED, MPFA_ERR_WORKSPACE, MPFA_ERR_HIP = range(5)
-SMOOTH, COMPUTE_STATS, TSCALE_UNIT, SEED_INIT, MXFP4 = 1, 2, 4, 8, 16
+SMOOTH, COMPUTE_STATS, TSCALE_UNIT, SEED_INIT, MXFP4, SEED_ELEMWISE = 1, 2, 4, 8, 16, 32
 HEAD_DIM, PAGE, TILE = 128, 64, 128
 
 EXPORTED = ("mpfa_quantize_qk", "mpfa_prefill", "mpfa_decode_workspace_size",

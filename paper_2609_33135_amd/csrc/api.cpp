@@ -90,7 +90,8 @@ mpfa_status mpfa_prefill(const mpfa_prefill_args* a, mpfa_stream_t stream) {
   if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
   if (a->batch < 1 || a->max_seqlen_q < 0 || a->max_pages < 1) return MPFA_ERR_INVALID;
   if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
-  if (a->flags & ~(MPFA_SMOOTH | MPFA_SEED_INIT | MPFA_MXFP4)) return MPFA_ERR_INVALID;
+  if (a->flags & ~(MPFA_SMOOTH | MPFA_SEED_INIT | MPFA_SEED_ELEMWISE | MPFA_MXFP4)) return MPFA_ERR_INVALID;
+  if ((a->flags & MPFA_SEED_INIT) && (a->flags & MPFA_SEED_ELEMWISE)) return MPFA_ERR_INVALID;
   const bool smooth = a->flags & MPFA_SMOOTH;
   if (!a->cu_seqlens_q || !a->q_start || !a->kv_len || !a->page_table || !a->q_codes ||
       !a->q_scales || !a->q_tscale || !a->k_codes || !a->k_scales || !a->v_codes ||
@@ -107,6 +108,7 @@ mpfa_status mpfa_prefill(const mpfa_prefill_args* a, mpfa_stream_t stream) {
   p.n_qtiles = (int)n_qtiles;
   p.smooth = smooth;
   p.seed_init = (a->flags & MPFA_SEED_INIT) != 0;
+  p.seed_elem = (a->flags & MPFA_SEED_ELEMWISE) != 0;
   p.mx = (a->flags & MPFA_MXFP4) != 0;
   p.xcd_remap = (a->h_kv % 8) == 0;
   p.lam = kLambda;

@@ -36,6 +36,7 @@ struct PrefillParams {
   int n_qtiles;     // max query tiles of one sequence
   int smooth;
   int seed_init;    // 1: compensation loaded as the accumulator input, 0: rank-one MFMA
+  int seed_elem;    // 1: compensation added to each score after the QK product
   int mx;           // Q/K in MXFP4: QK on the scaled FP4 MFMA
   int xcd_remap;    // 1: spread KV heads over the 8 XCDs (needs h_kv % 8 == 0)
   float lam;        // log2(e) / sqrt(128)

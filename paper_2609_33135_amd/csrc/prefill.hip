@@ -148,8 +148,12 @@ __device__ __forceinline__ void store_tile(PrefillSmem& sm, const TileRegs& r, f
 //  kSeedInit  the same rank-one matrix loaded directly as the accumulator input
 //             of the first FP16 MFMA (bit-identical: both start the accumulator
 //             at the FP32 value of the BF16 Delta_S);
-//  kSeedNone  no compensation (the unsmoothed "direct" variant).
-enum SeedMode { kSeedNone = 0, kSeedMfma = 1, kSeedInit = 2 };
+//  kSeedNone  no compensation (the unsmoothed "direct" variant);
+//  kSeedElem  the placement the rank-one seed replaces (Sec. 3.2, Fig. 10):
+//             the accumulator starts at zero and Delta_S is added to every
+//             score in FP32 after the QK product, on the softmax path.  Same
+//             values up to the FP32 rounding order.
+enum SeedMode { kSeedNone = 0, kSeedMfma = 1, kSeedInit = 2, kSeedElem = 3 };
 
 template <int SEED, bool MX>
 __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
@@ -299,6 +303,18 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
             }
           }
       }
+      if (SEED == kSeedElem) {
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb)
+#pragma unroll
+          for (int mb = 0; mb < 8; ++mb) {
+            const uint2 d4 = *reinterpret_cast<const uint2*>(&sm.ds[32 * g + 4 * mb]);
+            s[mb][nb][0] += __uint_as_float(d4.x << 16);
+            s[mb][nb][1] += __uint_as_float(d4.x & 0xFFFF0000u);
+            s[mb][nb][2] += __uint_as_float(d4.y << 16);
+            s[mb][nb][3] += __uint_as_float(d4.y & 0xFFFF0000u);
+          }
+      }
       if (need_mask) {
 #pragma unroll
         for (int mb = 0; mb < 8; ++mb)
@@ -390,10 +406,12 @@ hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream) {
   if (p.mx) {
     if (!p.smooth) prefill_kernel<kSeedNone, true><<<grid, block, 0, stream>>>(p);
     else if (p.seed_init) prefill_kernel<kSeedInit, true><<<grid, block, 0, stream>>>(p);
+    else if (p.seed_elem) prefill_kernel<kSeedElem, true><<<grid, block, 0, stream>>>(p);
     else prefill_kernel<kSeedMfma, true><<<grid, block, 0, stream>>>(p);
   } else {
     if (!p.smooth) prefill_kernel<kSeedNone, false><<<grid, block, 0, stream>>>(p);
     else if (p.seed_init) prefill_kernel<kSeedInit, false><<<grid, block, 0, stream>>>(p);
+    else if (p.seed_elem) prefill_kernel<kSeedElem, false><<<grid, block, 0, stream>>>(p);
     else prefill_kernel<kSeedMfma, false><<<grid, block, 0, stream>>>(p);
   }
   return hipGetLastError();

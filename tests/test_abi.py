@@ -57,7 +57,7 @@ def _prefill_args(mp, **kw):
 
 @pytest.mark.parametrize("field,value,status", [
     ("head_dim", 64, 2), ("head_dim", 0, 1), ("h_q", 7, 1), ("h_kv", 0, 1), ("batch", 0, 1),
-    ("max_pages", 0, 1), ("flags", 32, 1), ("q_codes", None, 1), ("ds", None, 1),
+    ("max_pages", 0, 1), ("flags", 64, 1), ("flags", 1 | 8 | 32, 1), ("q_codes", None, 1), ("ds", None, 1),
     ("max_seqlen_q", -1, 1), ("h_kv", 64, 1),
 ])
 def test_prefill_validation(mp, field, value, status):

@@ -114,6 +114,23 @@ def test_prefill_seed_modes_bit_identical(orc, mp):
     assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("mx", [False, True])
+def test_prefill_elementwise_placement(orc, mp, mx):
+    """The element-wise compensation placement (Fig. 10's comparison arm): every
+    output row against the oracle, and within one BF16 step of the seeded
+    placement (the two differ only in the FP32 rounding order of the scores)."""
+    print(f"case: element-wise placement mx={mx}", flush=True)
+    seqlens = [1, 130, 300, 513]
+    run = H.Run(orc, mp, 23, seqlens, 8, 2, outliers=True, mxfp4=mx)
+    out = run.prefill_gpu(extra_flags=mp.SEED_ELEMWISE)
+    _check(run, out, _all_items(seqlens, 8), label=f"elementwise mx={mx}")
+    seeded = H.bf16_f64(run.prefill_gpu())
+    ew = H.bf16_f64(out)
+    assert np.all(np.abs(ew - seeded) <= H.bf16_ulp(np.maximum(np.abs(ew), np.abs(seeded))))
+    for _ in range(4):
+        assert np.array_equal(run.prefill_gpu(extra_flags=mp.SEED_ELEMWISE), out)
+
+
 def test_prefill_repeatable_all_modes(orc, mp):
     """Every seed mode gives bit-identical outputs over repeated launches (a
     missing synchronisation or an unsatisfied hardware hazard shows up as
