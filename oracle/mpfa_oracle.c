@@ -310,6 +310,37 @@ void orc_mxfp4_dequant_row(const uint8_t* codes64, const uint8_t* scales8, doubl
  * and query head (Eq. 9) as an FP32 fused multiply-add chain over the
  * channels, rounded to BF16 (the compensation is carried in BF16, Sec. 7.4).
  * Query head h uses KV head h / (h_q / h_kv). */
+/* V as NVFP4 along keys (characterization of Sec. 3.1): for every page a
+ * sequence of this call occupies and every (KV head, channel), the page's 64
+ * values (absent slots as zero) form four 16-key groups, quantized with the
+ * same group rule as Q/K rows (Eq. 1) and tensor scale 1.  The row quantizer
+ * takes 8 groups; the page fills the first four. */
+static void nvfp4_v_pages(const orc_quant_args* a)
+{
+    const int Hkv = a->h_kv;
+    uint8_t* aux = (uint8_t*)a->v_aux;
+    for (int b = 0; b < a->batch; ++b) {
+        int64_t t0 = a->cu_seqlens[b], n = a->cu_seqlens[b + 1] - t0;
+        for (int64_t p0 = 0; p0 < n; p0 += ORC_PAGE) {
+            int64_t page = a->slot_mapping[t0 + p0] / ORC_PAGE;
+            int64_t cnt = n - p0 < ORC_PAGE ? n - p0 : ORC_PAGE;
+            for (int h = 0; h < Hkv; ++h) {
+                for (int c = 0; c < ORC_D; ++c) {
+                    float vals[ORC_D];
+                    uint8_t codes[64], scales[8];
+                    for (int j = 0; j < ORC_D; ++j) vals[j] = 0.0f;
+                    for (int64_t j = 0; j < cnt; ++j)
+                        vals[j] = orc_bf16_value(a->v[((t0 + p0 + j) * Hkv + h) * ORC_D + c]);
+                    orc_nvfp4_row(vals, 1.0f, codes, scales);
+                    uint8_t* dst = aux + ((page * Hkv + h) * ORC_D + c) * 36;
+                    memcpy(dst, codes, 32);
+                    memcpy(dst + 32, scales, 4);
+                }
+            }
+        }
+    }
+}
+
 int orc_quantize_qk(const orc_quant_args* a)
 {
     const int B = a->batch, Hq = a->h_q, Hkv = a->h_kv;
@@ -339,6 +370,19 @@ int orc_quantize_qk(const orc_quant_args* a)
                 orc_stats_one(x, n, (int64_t)Hkv * ORC_D, smooth, tunit,
                               a->k_mean + ((int64_t)b * Hkv + h) * ORC_D,
                               &a->k_tscale[(int64_t)b * Hkv + h]);
+            }
+        }
+    }
+
+    const int pv_bf16 = (a->flags & ORC_PV_BF16) != 0, pv_nv = (a->flags & ORC_PV_NVFP4) != 0;
+    if (pv_bf16 && pv_nv) return -1;
+    if ((pv_bf16 || pv_nv) && !a->v_aux) return -1;
+    if (pv_nv) {   /* fresh-prefill layout: token i of a sequence at slot i % 64 of its page */
+        for (int b = 0; b < B; ++b) {
+            int64_t t0 = a->cu_seqlens[b], n = a->cu_seqlens[b + 1] - t0;
+            for (int64_t i = 0; i < n; ++i) {
+                int64_t first = a->slot_mapping[t0 + i - i % ORC_PAGE];
+                if (first % ORC_PAGE != 0 || a->slot_mapping[t0 + i] != first + i % ORC_PAGE) return -2;
             }
         }
     }
@@ -378,6 +422,9 @@ int orc_quantize_qk(const orc_quant_args* a)
                 for (int c = 0; c < ORC_D; ++c)
                     a->v_codes[((page * Hkv + h) * ORC_D + c) * ORC_PAGE + off] =
                         orc_e4m3_encode((double)orc_bf16_value(vx[c]));
+                if (pv_bf16)
+                    for (int c = 0; c < ORC_D; ++c)
+                        ((uint16_t*)a->v_aux)[((page * Hkv + h) * ORC_D + c) * ORC_PAGE + off] = vx[c];
             }
             if (smooth) {
                 for (int h = 0; h < Hq; ++h) {
@@ -390,6 +437,7 @@ int orc_quantize_qk(const orc_quant_args* a)
             }
         }
     }
+    if (pv_nv) nvfp4_v_pages(a);
     return 0;
 }
 
@@ -427,8 +475,10 @@ void orc_visit(orc_state* st, const double* qd, const double* kd, const double* 
     if (key_hi <= key_lo) return;
     const double lam = lambda_d();
     const int quant_p = (flags & ORC_QUANT_P) != 0;
+    const int p_bf16 = (flags & ORC_P_BF16) != 0, p_nv = (flags & ORC_P_NVFP4) != 0;
     int64_t first = key_lo / tile, last = (key_hi - 1) / tile;
     double* s = (double*)malloc(sizeof(double) * (size_t)tile);
+    double* w_nv = (double*)malloc(sizeof(double) * (size_t)tile);
     for (int64_t it = 0; it <= last - first; ++it) {
         int64_t j = (flags & ORC_REVERSE) ? last - it : first + it;
         int64_t lo = j * tile > key_lo ? j * tile : key_lo;
@@ -449,12 +499,33 @@ void orc_visit(orc_state* st, const double* qd, const double* kd, const double* 
         double l_add = 0.0;
         double o_add[ORC_D];
         for (int c = 0; c < ORC_D; ++c) o_add[c] = 0.0;
+        if (p_nv) {
+            /* P' = 2688 P (the largest P, 1, maps to 6 * 448), then one NVFP4
+             * group per 16 keys aligned to multiples of 16 (Eq. 1, tensor scale
+             * 1): scale = E4M3(amax / 6), weight = scale * E2M1(P' / scale). */
+            for (int64_t key = lo; key < hi; ++key) {
+                double v = s[key - lo];
+                w_nv[key - lo] = v == -INFINITY ? 0.0 : 2688.0 * exp2(lam * (v - m_new));
+            }
+            for (int64_t g0 = lo - lo % 16; g0 < hi; g0 += 16) {
+                int64_t a0 = g0 > lo ? g0 : lo, a1 = g0 + 16 < hi ? g0 + 16 : hi;
+                double amax = 0.0;
+                for (int64_t key = a0; key < a1; ++key)
+                    if (w_nv[key - lo] > amax) amax = w_nv[key - lo];
+                double sd = orc_e4m3_value(orc_e4m3_encode(amax / 6.0));
+                for (int64_t key = a0; key < a1; ++key)
+                    w_nv[key - lo] = sd == 0.0 ? 0.0 : sd * orc_e2m1_value(orc_e2m1_encode(w_nv[key - lo] / sd));
+            }
+        }
         for (int64_t key = lo; key < hi; ++key) {
             double v = s[key - lo];
             if (v == -INFINITY) continue;
             double p = exp2(lam * (v - m_new));
             l_add += p;
-            double w = quant_p ? orc_e4m3_value(orc_e4m3_encode(448.0 * p)) : p;
+            double w = quant_p ? orc_e4m3_value(orc_e4m3_encode(448.0 * p))
+                     : p_bf16  ? (double)orc_bf16_value(orc_bf16_encode_f64(p))
+                     : p_nv    ? w_nv[key - lo]
+                               : p;
             if (w == 0.0) continue;
             const double* vr = vd + key * ORC_D;
             for (int c = 0; c < ORC_D; ++c) o_add[c] += w * vr[c];
@@ -464,11 +535,12 @@ void orc_visit(orc_state* st, const double* qd, const double* kd, const double* 
         st->m = m_new;
     }
     free(s);
+    free(w_nv);
 }
 
 /* Log-sum-exp merge of split-KV partition states (Sec. 5.3), then the final
  * normalisation O / l (O / (448 l) when O carries 448-scaled P codes). */
-void orc_merge(const orc_state* parts, int n, double* out, int quant_p)
+void orc_merge(const orc_state* parts, int n, double* out, double p_scale)
 {
     const double lam = lambda_d();
     double M = -INFINITY;
@@ -484,7 +556,7 @@ void orc_merge(const orc_state* parts, int n, double* out, int quant_p)
         l += f * parts[p].l;
         for (int c = 0; c < ORC_D; ++c) o[c] += f * parts[p].o[c];
     }
-    double denom = (quant_p ? 448.0 : 1.0) * l;
+    double denom = p_scale * l;
     for (int c = 0; c < ORC_D; ++c) out[c] = o[c] / denom;
 }
 
@@ -504,7 +576,8 @@ void orc_attention_f64(const double* q, const double* k, const double* v,
             orc_visit(&st[p], q + r * ORC_D, k, v, ds ? ds + r * nk : NULL, q_pos[r], lo, hi,
                       tile, flags);
         }
-        orc_merge(st, (int)nparts, out + r * ORC_D, (flags & ORC_QUANT_P) != 0);
+        orc_merge(st, (int)nparts, out + r * ORC_D,
+                  (flags & ORC_QUANT_P) ? 448.0 : (flags & ORC_P_NVFP4) ? 2688.0 : 1.0);
         free(st);
     }
 }
@@ -553,9 +626,18 @@ static void gather_kv(const orc_cache* c, int b, int hk, int64_t n, double* kd, 
             orc_mxfp4_dequant_row(c->k_codes + row * 64, c->k_scales + row * 8, kd + key * ORC_D);
         else
             orc_nvfp4_dequant_row(c->k_codes + row * 64, c->k_scales + row * 8, tk, kd + key * ORC_D);
-        for (int d = 0; d < ORC_D; ++d)
-            vd[key * ORC_D + d] =
-                orc_e4m3_value(c->v_codes[((page * c->h_kv + hk) * ORC_D + d) * ORC_PAGE + off]);
+        for (int d = 0; d < ORC_D; ++d) {
+            int64_t vr = (page * c->h_kv + hk) * ORC_D + d;
+            if (c->flags & ORC_PV_BF16) {
+                vd[key * ORC_D + d] = orc_bf16_value(((const uint16_t*)c->v_aux)[vr * ORC_PAGE + off]);
+            } else if (c->flags & ORC_PV_NVFP4) {
+                const uint8_t* r = (const uint8_t*)c->v_aux + vr * 36;
+                uint8_t q = (uint8_t)((r[off / 2] >> (4 * (off % 2))) & 15);
+                vd[key * ORC_D + d] = orc_e4m3_value(r[32 + off / 16]) * orc_e2m1_value(q);
+            } else {
+                vd[key * ORC_D + d] = orc_e4m3_value(c->v_codes[vr * ORC_PAGE + off]);
+            }
+        }
     }
 }
 
@@ -588,6 +670,9 @@ static int run_items(const orc_cache* c, const int32_t* cu_seqlens, const int32_
 {
     const int grp = c->h_q / c->h_kv;
     const int smooth = (c->flags & ORC_SMOOTH) != 0;
+    /* P quantizer of the cache's precision assignment (Sec. 3.1) */
+    const int pmode = (c->flags & ORC_PV_BF16) ? ORC_P_BF16 : (c->flags & ORC_PV_NVFP4) ? ORC_P_NVFP4 : ORC_QUANT_P;
+    const double p_scale = pmode == ORC_QUANT_P ? 448.0 : pmode == ORC_P_NVFP4 ? 2688.0 : 1.0;
     item_key* keys = (item_key*)malloc(sizeof(item_key) * (size_t)(n_items > 0 ? n_items : 1));
     for (int64_t i = 0; i < n_items; ++i) {
         keys[i].b = item_b[i];
@@ -634,10 +719,10 @@ static int run_items(const orc_cache* c, const int32_t* cu_seqlens, const int32_
             for (int64_t p = 0; p < nparts; ++p) {
                 orc_state_init(&st[p]);
                 int64_t lo = p * part, hi = (p + 1) * part < n ? (p + 1) * part : n;
-                orc_visit(&st[p], qd, kd, vd, dsh, pos, lo, hi, 128, ORC_QUANT_P | ORC_REVERSE);
+                orc_visit(&st[p], qd, kd, vd, dsh, pos, lo, hi, 128, pmode | ORC_REVERSE);
             }
             double o[ORC_D];
-            orc_merge(st, (int)nparts, o, 1);
+            orc_merge(st, (int)nparts, o, p_scale);
             free(st);
             for (int d = 0; d < ORC_D; ++d) {
                 if (out_f64) out_f64[it * ORC_D + d] = o[d];

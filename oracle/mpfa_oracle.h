@@ -47,8 +47,16 @@ extern "C" {
 #define ORC_MXFP4         8   /* Q/K as MXFP4: E8M0 scale per 32, tensor scale 1
                                  (also set in orc_cache.flags for the attention) */
 
+#define ORC_PV_BF16      16   /* characterization of Sec. 3.1 / Fig. 3a: V kept in BF16
+                                 (cache array v_aux) and P rounded to BF16          */
+#define ORC_PV_NVFP4     32   /* characterization of Sec. 3.1 / Fig. 3a: V as NVFP4 in
+                                 16-key groups per channel (v_aux, tensor scale 1) and
+                                 P as NVFP4 with dynamic E4M3 scales per 16 keys     */
 #define ORC_QUANT_P       1   /* attention core: round 448*P to E4M3         */
 #define ORC_REVERSE       2   /* attention core: visit KV tiles last to first */
+#define ORC_P_BF16        4   /* attention core: round P to BF16 (no scale)  */
+#define ORC_P_NVFP4       8   /* attention core: 2688*P as NVFP4 per 16 keys aligned to
+                                 multiples of 16: E4M3 scale of amax/6, E2M1 codes  */
 
 /* ---- number formats (Sec. 2.1 Eq. 1, Sec. 4.1) ----------------------------- */
 double  orc_e2m1_value(uint8_t code);            /* code in 0..15, bit 3 = sign */
@@ -102,6 +110,13 @@ typedef struct {
     uint8_t* k_scales;              /* [pages][h_kv][64][8]                    */
     uint8_t* v_codes;               /* [pages][h_kv][128][64]  channel-major   */
     uint16_t* ds;                   /* bf16 [pages][h_q][64]; unused w/o smooth */
+    void*     v_aux;                /* ORC_PV_BF16: bf16 [pages][h_kv][128][64];
+                                       ORC_PV_NVFP4: u8 [pages][h_kv][128][36] (32 code
+                                       bytes, key 2i in the low nibble of byte i, then
+                                       4 E4M3 scales of keys 16j..16j+15).  NVFP4 needs
+                                       each sequence's tokens at slots 0, 1, 2, ... of
+                                       its pages in order (a fresh prefill); the call's
+                                       pages are written whole, absent slots as zero.  */
 } orc_quant_args;
 
 int orc_quantize_qk(const orc_quant_args* a);
@@ -122,8 +137,9 @@ void orc_visit(orc_state* st, const double* qd, const double* kd, const double* 
                const double* dsd, int64_t q_pos, int64_t key_lo, int64_t key_hi,
                int tile, int flags);
 
-/* Log-sum-exp merge of partition states, then divide (Sec. 5.3). */
-void orc_merge(const orc_state* parts, int n, double* out /*[128]*/, int quant_p);
+/* Log-sum-exp merge of partition states, then divide by p_scale * l, where
+ * p_scale is the factor the P quantizer applied (448, 2688 or 1) (Sec. 5.3). */
+void orc_merge(const orc_state* parts, int n, double* out /*[128]*/, double p_scale);
 
 /* Generic FP64 attention over contiguous arrays (used by the pins):
  * q [nq][128], k/v [nk][128], ds [nq][nk] or NULL, q_pos[nq] (keys > q_pos
@@ -140,7 +156,7 @@ void orc_attention_textbook(const double* q, const double* k, const double* v,
 
 /* ---- product-shaped attention over the quantized paged cache -------------- */
 typedef struct {
-    int32_t batch, h_q, h_kv, max_pages, flags;  /* flags: ORC_SMOOTH, ORC_MXFP4 */
+    int32_t batch, h_q, h_kv, max_pages, flags;  /* ORC_SMOOTH, ORC_MXFP4, ORC_PV_* */
     const int32_t*  page_table;   /* [batch][max_pages]                    */
     const int32_t*  kv_len;       /* [batch]                               */
     const uint8_t*  k_codes;      /* [pages][h_kv][64][64]                 */
@@ -151,6 +167,7 @@ typedef struct {
     const uint8_t*  q_codes;      /* [Tq][h_q][64]                         */
     const uint8_t*  q_scales;     /* [Tq][h_q][8]                          */
     const float*    q_tscale;     /* [batch][h_q]                          */
+    const void*     v_aux;        /* with ORC_PV_BF16 / ORC_PV_NVFP4 in flags */
 } orc_cache;
 
 /* Causal prefill over the paged cache for selected rows.

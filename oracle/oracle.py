@@ -21,8 +21,12 @@ SMOOTH = 1
 COMPUTE_STATS = 2
 TSCALE_UNIT = 4
 MXFP4 = 8
+PV_BF16 = 16        # V in BF16 (v_aux), P rounded to BF16
+PV_NVFP4 = 32       # V as NVFP4 along keys (v_aux), P as NVFP4 per 16 keys
 QUANT_P = 1
 REVERSE = 2
+P_BF16 = 4
+P_NVFP4 = 8
 
 D = 128
 PAGE = 64
@@ -49,7 +53,7 @@ class _QuantArgs(C.Structure):
                 ("q_mean", C.c_void_p), ("k_mean", C.c_void_p), ("k_tscale", C.c_void_p),
                 ("q_codes", C.c_void_p), ("q_scales", C.c_void_p), ("q_tscale", C.c_void_p),
                 ("k_codes", C.c_void_p), ("k_scales", C.c_void_p), ("v_codes", C.c_void_p),
-                ("ds", C.c_void_p)]
+                ("ds", C.c_void_p), ("v_aux", C.c_void_p)]
 
 
 class _Cache(C.Structure):
@@ -58,7 +62,8 @@ class _Cache(C.Structure):
                 ("page_table", C.c_void_p), ("kv_len", C.c_void_p),
                 ("k_codes", C.c_void_p), ("k_scales", C.c_void_p), ("v_codes", C.c_void_p),
                 ("ds", C.c_void_p), ("k_tscale", C.c_void_p),
-                ("q_codes", C.c_void_p), ("q_scales", C.c_void_p), ("q_tscale", C.c_void_p)]
+                ("q_codes", C.c_void_p), ("q_scales", C.c_void_p), ("q_tscale", C.c_void_p),
+                ("v_aux", C.c_void_p)]
 
 
 def lib():
@@ -240,6 +245,10 @@ def quantize_qk(q, k, v, cu_seqlens, slot_mapping, n_pages, flags,
             "v_codes": np.zeros((n_pages, Hkv, D, PAGE), np.uint8),
             "ds": np.zeros((n_pages, Hq, PAGE), np.uint16),
         }
+    if (flags & PV_BF16) and "v_aux" not in cache:
+        cache["v_aux"] = np.zeros((n_pages, Hkv, D, PAGE), np.uint16)
+    if (flags & PV_NVFP4) and "v_aux" not in cache:
+        cache["v_aux"] = np.zeros((n_pages, Hkv, D, 36), np.uint8)
     stats = flags & COMPUTE_STATS
     if stats:
         q_mean = np.zeros((B, Hq, D), np.uint16)
@@ -258,7 +267,7 @@ def quantize_qk(q, k, v, cu_seqlens, slot_mapping, n_pages, flags,
                    _p(q_mean), _p(k_mean), _p(k_tscale),
                    _p(out["q_codes"]), _p(out["q_scales"]), _p(out["q_tscale"]),
                    _p(cache["k_codes"]), _p(cache["k_scales"]), _p(cache["v_codes"]),
-                   _p(cache["ds"]))
+                   _p(cache["ds"]), _p(cache.get("v_aux")))
     rc = lib().orc_quantize_qk(C.byref(a))
     if rc != 0:
         raise ValueError("orc_quantize_qk rejected its arguments")
@@ -306,22 +315,26 @@ def _cache_struct(cache, page_table, kv_len, k_tscale, q_codes, q_scales, q_tsca
                 v_codes=_c(cache["v_codes"], np.uint8), ds=_c(cache["ds"], np.uint16),
                 k_tscale=_c(k_tscale, np.float32), q_codes=_c(q_codes, np.uint8),
                 q_scales=_c(q_scales, np.uint8), q_tscale=_c(q_tscale, np.float32), pt=pt, kl=kl)
+    if flags & (PV_BF16 | PV_NVFP4):
+        arrs["v_aux"] = np.ascontiguousarray(cache["v_aux"])
     keep.append(arrs)
     h_kv = arrs["k_codes"].shape[1]
     return _Cache(pt.shape[0], h_q, h_kv, pt.shape[1], flags, _p(pt), _p(kl),
                   _p(arrs["k_codes"]), _p(arrs["k_scales"]), _p(arrs["v_codes"]),
                   _p(arrs["ds"]), _p(arrs["k_tscale"]), _p(arrs["q_codes"]),
-                  _p(arrs["q_scales"]), _p(arrs["q_tscale"]))
+                  _p(arrs["q_scales"]), _p(arrs["q_tscale"]), _p(arrs.get("v_aux")))
 
 
 def prefill(cache, page_table, kv_len, k_tscale, q_codes, q_scales, q_tscale, cu_seqlens,
-            q_start, items, smooth=True, mxfp4=False):
+            q_start, items, smooth=True, mxfp4=False, pv=0):
     """items: int32 [n][3] rows of (sequence, row within sequence, q head).
+    pv: 0 (FP8 P and V), PV_BF16 or PV_NVFP4 (precision assignments of the PV
+    product compared in Sec. 3.1; the cache then carries v_aux).
     Returns (bf16 bits [n][128], float64 [n][128])."""
     keep = []
     h_q = q_codes.shape[1]
     cs = _cache_struct(cache, page_table, kv_len, k_tscale, q_codes, q_scales, q_tscale, h_q,
-                       (SMOOTH if smooth else 0) | (MXFP4 if mxfp4 else 0), keep)
+                       (SMOOTH if smooth else 0) | (MXFP4 if mxfp4 else 0) | pv, keep)
     items = _c(items, np.int32).reshape(-1, 3)
     ib, ir, ih = (np.ascontiguousarray(items[:, i]) for i in range(3))
     cu = _c(cu_seqlens, np.int32)

@@ -448,3 +448,162 @@ def test_mxfp4_prefill_matches_dequantized_reference(orc):
         ref = orc.attention_f64(qd[rows], kd, vd, np.tile(dsd, (len(rows), 1)), rows,
                                 tile=128, flags=orc.REVERSE | orc.QUANT_P)
         assert np.max(np.abs(a64[sel] - ref)) < 1e-12
+
+
+# ---------------------------------------------------------------------------
+# Precision assignments of the PV product (Sec. 3.1, Fig. 3a): P in BF16 or
+# NVFP4 (per 16 keys, dynamic E4M3 scales, P' = 2688 P), V in BF16 or NVFP4
+# along keys.  These are characterization arms next to the method's FP8 PV.
+# ---------------------------------------------------------------------------
+E4M3_POS = None
+
+
+def _e4m3_brute(x):
+    """Nearest positive E4M3 value to x >= 0 (ties to the even code), clipped to 448."""
+    global E4M3_POS
+    if E4M3_POS is None:
+        vals = []
+        for c in range(0x7F):
+            e, m = c >> 3, c & 7
+            vals.append((m / 8.0) * 2.0 ** -6 if e == 0 else (1 + m / 8.0) * 2.0 ** (e - 7))
+        E4M3_POS = np.array(vals)
+    x = min(float(x), 448.0)
+    d = np.abs(E4M3_POS - x)
+    cand = np.flatnonzero(d == d.min())
+    c = int(cand[0]) if len(cand) == 1 else int([k for k in cand if k % 2 == 0][0])
+    return E4M3_POS[c]
+
+
+def _p_nvfp4_weights(p):
+    """Brute-force NVFP4 weights of 2688 * p over 16-element groups."""
+    pp = 2688.0 * np.asarray(p, np.float64)
+    w = np.zeros_like(pp)
+    for g0 in range(0, len(pp), 16):
+        grp = pp[g0:g0 + 16]
+        sd = _e4m3_brute(grp.max() / 6.0)
+        if sd == 0.0:
+            continue
+        for i, y in enumerate(grp):
+            w[g0 + i] = sd * E2M1_GRID[_mx_brute(y / sd) & 7]
+    return w
+
+
+@pytest.mark.parametrize("mode", ["bf16", "nvfp4"])
+def test_pv_precision_single_key_and_uniform(orc, mode):
+    """One visible key returns its V row exactly; equal scores return the plain
+    mean of V (every weight is the same code)."""
+    flag = orc.P_BF16 if mode == "bf16" else orc.P_NVFP4
+    rng = np.random.default_rng(3)
+    k = rng.standard_normal((70, 128))
+    v = rng.standard_normal((70, 128))
+    q = rng.standard_normal((1, 128))
+    o = orc.attention_f64(q, k, v, q_pos=np.array([0]), flags=orc.REVERSE | flag)
+    assert np.allclose(o[0], v[0], rtol=2.0 ** -51, atol=0)   # (2688 v) / 2688: two FP64 roundings
+    o = orc.attention_f64(np.zeros((1, 128)), k, v, flags=orc.REVERSE | flag)
+    assert np.allclose(o[0], v.mean(axis=0), rtol=0, atol=1e-13)
+
+
+def test_pv_bf16_error_bound(orc):
+    """Rounding each weight to BF16 (relative error <= 2^-9) moves the output by
+    at most 2^-9 max|V| from the unquantized FP64 result."""
+    rng = np.random.default_rng(4)
+    for _ in range(5):
+        k = rng.standard_normal((300, 128)) * 2
+        v = rng.standard_normal((300, 128))
+        q = rng.standard_normal((6, 128)) * 2
+        a = orc.attention_f64(q, k, v, flags=orc.REVERSE | orc.P_BF16)
+        b = orc.attention_f64(q, k, v, flags=orc.REVERSE)
+        assert np.max(np.abs(a - b)) <= 2.0 ** -9 * np.max(np.abs(v)) * 1.0001
+
+
+def test_pv_nvfp4_group_rule_brute_force(orc):
+    """One 128-key tile: the weights follow the per-16-key NVFP4 rule exactly
+    (brute-force nearest grid values), the normaliser is the unquantized sum."""
+    rng = np.random.default_rng(5)
+    for trial in range(6):
+        n = [128, 100, 37, 16, 1, 77][trial]
+        k = rng.standard_normal((n, 128)) * rng.uniform(0.5, 3)
+        v = rng.standard_normal((n, 128))
+        q = rng.standard_normal((1, 128))
+        o = orc.attention_f64(q, k, v, flags=orc.REVERSE | orc.P_NVFP4)[0]
+        s = (k @ q[0]) * LAM
+        p = np.exp2(s - s.max())
+        w = _p_nvfp4_weights(p)
+        want = (w @ v) / (2688.0 * p.sum())
+        assert np.max(np.abs(o - want)) < 1e-12, trial
+
+
+def _pv_quant(orc, seed, n, pv, shuffle=True):
+    q = W.gen_tensor(seed, W.STREAM_Q, 0, 0, n, 2, outliers=True, out_stream=W.STREAM_OUT_Q)
+    k = W.gen_tensor(seed, W.STREAM_K, 0, 0, n, 1, outliers=True, out_stream=W.STREAM_OUT_K,
+                     offset=W.k_offsets(seed, 1))
+    v = W.gen_tensor(seed, W.STREAM_V, 0, 0, n, 1)
+    qb, kb, vb = (t.view(torch.int16).numpy().view(np.uint16) for t in (q, k, v))
+    pt, n_pages = W.make_pages(seed, [n], shuffle)
+    slots = W.slots_for(pt, 0, np.arange(n))
+    r = orc.quantize_qk(qb, kb, vb, [0, n], slots, n_pages, orc.SMOOTH | orc.COMPUTE_STATS | pv)
+    return qb, kb, vb, pt, r
+
+
+def test_pv_cache_layouts(orc):
+    """v_aux holds V's BF16 bits channel-major, or per (page, channel) four
+    NVFP4 groups of 16 keys equal to the row quantizer on the page's values
+    (absent slots zero); a token off the fresh-prefill layout is refused."""
+    n = 150
+    qb, kb, vb, pt, r = _pv_quant(orc, 41, n, orc.PV_BF16)
+    aux = r["cache"]["v_aux"]
+    for j in range(n):
+        page, off = pt[0, j // 64], j % 64
+        assert np.array_equal(aux[page, 0, :, off], vb.reshape(n, 1, 128)[j, 0])
+    qb, kb, vb, pt, r = _pv_quant(orc, 41, n, orc.PV_NVFP4)
+    aux = r["cache"]["v_aux"]
+    vf = bits_to_f64(vb).reshape(n, 128)
+    for lp in range(3):
+        page = pt[0, lp]
+        cnt = min(64, n - 64 * lp)
+        for c in range(0, 128, 7):
+            vals = np.zeros(128, np.float32)
+            vals[:cnt] = vf[64 * lp:64 * lp + cnt, c]
+            codes, scales = orc.nvfp4_row(vals, 1.0)
+            assert np.array_equal(aux[page, 0, c, :32], codes[:32])
+            assert np.array_equal(aux[page, 0, c, 32:], scales[:4])
+    bad = W.slots_for(pt, 0, np.arange(n)).copy()
+    bad[[3, 4]] = bad[[4, 3]]
+    with pytest.raises(ValueError):
+        orc.quantize_qk(qb, kb, vb, [0, n], bad, 3, orc.SMOOTH | orc.COMPUTE_STATS | orc.PV_NVFP4)
+
+
+@pytest.mark.parametrize("pv", ["bf16", "nvfp4"])
+def test_pv_prefill_matches_dequantized_reference(orc, pv):
+    """The paged prefill in a PV precision mode equals the FP64 attention core
+    over the dequantized arrays with the matching P quantizer."""
+    flag = orc.PV_BF16 if pv == "bf16" else orc.PV_NVFP4
+    pflag = orc.P_BF16 if pv == "bf16" else orc.P_NVFP4
+    n = 300
+    qb, kb, vb, pt, r = _pv_quant(orc, 43, n, flag)
+    items = np.array([(0, i, h) for i in range(0, n, 7) for h in range(2)], np.int32)
+    _, o64 = orc.prefill(r["cache"], pt, [n], r["k_tscale"], r["q_codes"], r["q_scales"],
+                         r["q_tscale"], [0, n], [0], items, pv=flag)
+    kd = np.stack([orc.nvfp4_dequant_row(r["cache"]["k_codes"][pt[0, j // 64], 0, j % 64],
+                                         r["cache"]["k_scales"][pt[0, j // 64], 0, j % 64],
+                                         r["k_tscale"][0, 0]) for j in range(n)])
+    aux = r["cache"]["v_aux"]
+    if pv == "bf16":
+        vd = np.stack([bits_to_f64(aux[pt[0, j // 64], 0, :, j % 64]) for j in range(n)])
+    else:
+        vd = np.zeros((n, 128))
+        for j in range(n):
+            row = aux[pt[0, j // 64], 0, :, :]
+            off = j % 64
+            codes = (row[:, off // 2] >> (4 * (off % 2))) & 15
+            vd[j] = np.array([orc.e4m3_value(int(row[c, 32 + off // 16])) * orc.e2m1_value(int(codes[c]))
+                              for c in range(128)])
+    for h in range(2):
+        qd = np.stack([orc.nvfp4_dequant_row(r["q_codes"][i, h], r["q_scales"][i, h],
+                                             r["q_tscale"][0, h]) for i in range(n)])
+        ds = bits_to_f64(r["cache"]["ds"][:, h, :][pt[0]].reshape(-1)[:n])
+        sel = items[:, 2] == h
+        rows = items[sel, 1]
+        ref = orc.attention_f64(qd[rows], kd, vd, np.tile(ds, (len(rows), 1)), rows,
+                                tile=128, flags=orc.REVERSE | pflag)
+        assert np.max(np.abs(o64[sel] - ref)) < 1e-12
