@@ -315,10 +315,11 @@ void orc_mxfp4_dequant_row(const uint8_t* codes64, const uint8_t* scales8, doubl
  * values (absent slots as zero) form four 16-key groups, quantized with the
  * same group rule as Q/K rows (Eq. 1) and tensor scale 1.  The row quantizer
  * takes 8 groups; the page fills the first four. */
-static void nvfp4_v_pages(const orc_quant_args* a)
+static void nvfp4_v_pages(const orc_quant_args* a, int64_t n_pages)
 {
     const int Hkv = a->h_kv;
     uint8_t* aux = (uint8_t*)a->v_aux;
+    uint8_t* aux_scales = aux + n_pages * Hkv * ORC_D * 32;
     for (int b = 0; b < a->batch; ++b) {
         int64_t t0 = a->cu_seqlens[b], n = a->cu_seqlens[b + 1] - t0;
         for (int64_t p0 = 0; p0 < n; p0 += ORC_PAGE) {
@@ -332,9 +333,9 @@ static void nvfp4_v_pages(const orc_quant_args* a)
                     for (int64_t j = 0; j < cnt; ++j)
                         vals[j] = orc_bf16_value(a->v[((t0 + p0 + j) * Hkv + h) * ORC_D + c]);
                     orc_nvfp4_row(vals, 1.0f, codes, scales);
-                    uint8_t* dst = aux + ((page * Hkv + h) * ORC_D + c) * 36;
-                    memcpy(dst, codes, 32);
-                    memcpy(dst + 32, scales, 4);
+                    const int64_t r = (page * Hkv + h) * ORC_D + c;
+                    memcpy(aux + r * 32, codes, 32);
+                    memcpy(aux_scales + r * 4, scales, 4);
                 }
             }
         }
@@ -437,7 +438,7 @@ int orc_quantize_qk(const orc_quant_args* a)
             }
         }
     }
-    if (pv_nv) nvfp4_v_pages(a);
+    if (pv_nv) nvfp4_v_pages(a, a->num_pages);
     return 0;
 }
 
@@ -631,9 +632,10 @@ static void gather_kv(const orc_cache* c, int b, int hk, int64_t n, double* kd, 
             if (c->flags & ORC_PV_BF16) {
                 vd[key * ORC_D + d] = orc_bf16_value(((const uint16_t*)c->v_aux)[vr * ORC_PAGE + off]);
             } else if (c->flags & ORC_PV_NVFP4) {
-                const uint8_t* r = (const uint8_t*)c->v_aux + vr * 36;
-                uint8_t q = (uint8_t)((r[off / 2] >> (4 * (off % 2))) & 15);
-                vd[key * ORC_D + d] = orc_e4m3_value(r[32 + off / 16]) * orc_e2m1_value(q);
+                const uint8_t* codes = (const uint8_t*)c->v_aux + vr * 32;
+                const uint8_t* sc = (const uint8_t*)c->v_aux + c->num_pages * c->h_kv * ORC_D * 32 + vr * 4;
+                uint8_t q = (uint8_t)((codes[off / 2] >> (4 * (off % 2))) & 15);
+                vd[key * ORC_D + d] = orc_e4m3_value(sc[off / 16]) * orc_e2m1_value(q);
             } else {
                 vd[key * ORC_D + d] = orc_e4m3_value(c->v_codes[vr * ORC_PAGE + off]);
             }

@@ -111,12 +111,14 @@ typedef struct {
     uint8_t* v_codes;               /* [pages][h_kv][128][64]  channel-major   */
     uint16_t* ds;                   /* bf16 [pages][h_q][64]; unused w/o smooth */
     void*     v_aux;                /* ORC_PV_BF16: bf16 [pages][h_kv][128][64];
-                                       ORC_PV_NVFP4: u8 [pages][h_kv][128][36] (32 code
-                                       bytes, key 2i in the low nibble of byte i, then
-                                       4 E4M3 scales of keys 16j..16j+15).  NVFP4 needs
+                                       ORC_PV_NVFP4: a code plane u8 [pages][h_kv][128][32]
+                                       (key 2i in the low nibble of byte i) followed by
+                                       a scale plane u8 [pages][h_kv][128][4] (E4M3 of
+                                       keys 16j..16j+15).  NVFP4 needs
                                        each sequence's tokens at slots 0, 1, 2, ... of
                                        its pages in order (a fresh prefill); the call's
                                        pages are written whole, absent slots as zero.  */
+    int64_t   num_pages;            /* cache capacity in pages (plane size of v_aux)    */
 } orc_quant_args;
 
 int orc_quantize_qk(const orc_quant_args* a);
@@ -168,6 +170,7 @@ typedef struct {
     const uint8_t*  q_scales;     /* [Tq][h_q][8]                          */
     const float*    q_tscale;     /* [batch][h_q]                          */
     const void*     v_aux;        /* with ORC_PV_BF16 / ORC_PV_NVFP4 in flags */
+    int64_t         num_pages;    /* cache capacity in pages (plane size of v_aux) */
 } orc_cache;
 
 /* Causal prefill over the paged cache for selected rows.

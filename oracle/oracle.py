@@ -53,7 +53,7 @@ class _QuantArgs(C.Structure):
                 ("q_mean", C.c_void_p), ("k_mean", C.c_void_p), ("k_tscale", C.c_void_p),
                 ("q_codes", C.c_void_p), ("q_scales", C.c_void_p), ("q_tscale", C.c_void_p),
                 ("k_codes", C.c_void_p), ("k_scales", C.c_void_p), ("v_codes", C.c_void_p),
-                ("ds", C.c_void_p), ("v_aux", C.c_void_p)]
+                ("ds", C.c_void_p), ("v_aux", C.c_void_p), ("num_pages", C.c_int64)]
 
 
 class _Cache(C.Structure):
@@ -63,7 +63,7 @@ class _Cache(C.Structure):
                 ("k_codes", C.c_void_p), ("k_scales", C.c_void_p), ("v_codes", C.c_void_p),
                 ("ds", C.c_void_p), ("k_tscale", C.c_void_p),
                 ("q_codes", C.c_void_p), ("q_scales", C.c_void_p), ("q_tscale", C.c_void_p),
-                ("v_aux", C.c_void_p)]
+                ("v_aux", C.c_void_p), ("num_pages", C.c_int64)]
 
 
 def lib():
@@ -222,6 +222,13 @@ def stats_one(x_bf16, smooth=True, tscale_unit=False):
 
 # ---- quantization pass --------------------------------------------------------
 
+def v_aux_nvfp4_planes(aux, n_pages, h_kv):
+    """Views of an NVFP4 v_aux buffer: codes [pages][h_kv][128][32] and
+    E4M3 scales [pages][h_kv][128][4]."""
+    n = n_pages * h_kv * D
+    return aux[:n * 32].reshape(n_pages, h_kv, D, 32), aux[n * 32:n * 36].reshape(n_pages, h_kv, D, 4)
+
+
 def quantize_qk(q, k, v, cu_seqlens, slot_mapping, n_pages, flags,
                 q_mean=None, k_mean=None, k_tscale=None, cache=None):
     """q: uint16 [T][Hq][128], k/v: uint16 [T][Hkv][128] (bf16 bits).
@@ -248,7 +255,8 @@ def quantize_qk(q, k, v, cu_seqlens, slot_mapping, n_pages, flags,
     if (flags & PV_BF16) and "v_aux" not in cache:
         cache["v_aux"] = np.zeros((n_pages, Hkv, D, PAGE), np.uint16)
     if (flags & PV_NVFP4) and "v_aux" not in cache:
-        cache["v_aux"] = np.zeros((n_pages, Hkv, D, 36), np.uint8)
+        # code plane [pages][Hkv][128][32], then scale plane [pages][Hkv][128][4]
+        cache["v_aux"] = np.zeros(n_pages * Hkv * D * 36, np.uint8)
     stats = flags & COMPUTE_STATS
     if stats:
         q_mean = np.zeros((B, Hq, D), np.uint16)
@@ -267,7 +275,7 @@ def quantize_qk(q, k, v, cu_seqlens, slot_mapping, n_pages, flags,
                    _p(q_mean), _p(k_mean), _p(k_tscale),
                    _p(out["q_codes"]), _p(out["q_scales"]), _p(out["q_tscale"]),
                    _p(cache["k_codes"]), _p(cache["k_scales"]), _p(cache["v_codes"]),
-                   _p(cache["ds"]), _p(cache.get("v_aux")))
+                   _p(cache["ds"]), _p(cache.get("v_aux")), cache["k_codes"].shape[0])
     rc = lib().orc_quantize_qk(C.byref(a))
     if rc != 0:
         raise ValueError("orc_quantize_qk rejected its arguments")
@@ -322,7 +330,8 @@ def _cache_struct(cache, page_table, kv_len, k_tscale, q_codes, q_scales, q_tsca
     return _Cache(pt.shape[0], h_q, h_kv, pt.shape[1], flags, _p(pt), _p(kl),
                   _p(arrs["k_codes"]), _p(arrs["k_scales"]), _p(arrs["v_codes"]),
                   _p(arrs["ds"]), _p(arrs["k_tscale"]), _p(arrs["q_codes"]),
-                  _p(arrs["q_scales"]), _p(arrs["q_tscale"]), _p(arrs.get("v_aux")))
+                  _p(arrs["q_scales"]), _p(arrs["q_tscale"]), _p(arrs.get("v_aux")),
+                  arrs["k_codes"].shape[0])
 
 
 def prefill(cache, page_table, kv_len, k_tscale, q_codes, q_scales, q_tscale, cu_seqlens,

@@ -556,7 +556,7 @@ def test_pv_cache_layouts(orc):
         page, off = pt[0, j // 64], j % 64
         assert np.array_equal(aux[page, 0, :, off], vb.reshape(n, 1, 128)[j, 0])
     qb, kb, vb, pt, r = _pv_quant(orc, 41, n, orc.PV_NVFP4)
-    aux = r["cache"]["v_aux"]
+    codes_p, scales_p = orc.v_aux_nvfp4_planes(r["cache"]["v_aux"], r["cache"]["k_codes"].shape[0], 1)
     vf = bits_to_f64(vb).reshape(n, 128)
     for lp in range(3):
         page = pt[0, lp]
@@ -565,8 +565,8 @@ def test_pv_cache_layouts(orc):
             vals = np.zeros(128, np.float32)
             vals[:cnt] = vf[64 * lp:64 * lp + cnt, c]
             codes, scales = orc.nvfp4_row(vals, 1.0)
-            assert np.array_equal(aux[page, 0, c, :32], codes[:32])
-            assert np.array_equal(aux[page, 0, c, 32:], scales[:4])
+            assert np.array_equal(codes_p[page, 0, c], codes[:32])
+            assert np.array_equal(scales_p[page, 0, c], scales[:4])
     bad = W.slots_for(pt, 0, np.arange(n)).copy()
     bad[[3, 4]] = bad[[4, 3]]
     with pytest.raises(ValueError):
@@ -591,12 +591,12 @@ def test_pv_prefill_matches_dequantized_reference(orc, pv):
     if pv == "bf16":
         vd = np.stack([bits_to_f64(aux[pt[0, j // 64], 0, :, j % 64]) for j in range(n)])
     else:
+        codes_p, scales_p = orc.v_aux_nvfp4_planes(aux, r["cache"]["k_codes"].shape[0], 1)
         vd = np.zeros((n, 128))
         for j in range(n):
-            row = aux[pt[0, j // 64], 0, :, :]
-            off = j % 64
-            codes = (row[:, off // 2] >> (4 * (off % 2))) & 15
-            vd[j] = np.array([orc.e4m3_value(int(row[c, 32 + off // 16])) * orc.e2m1_value(int(codes[c]))
+            page, off = pt[0, j // 64], j % 64
+            codes = (codes_p[page, 0, :, off // 2] >> (4 * (off % 2))) & 15
+            vd[j] = np.array([orc.e4m3_value(int(scales_p[page, 0, c, off // 16])) * orc.e2m1_value(int(codes[c]))
                               for c in range(128)])
     for h in range(2):
         qd = np.stack([orc.nvfp4_dequant_row(r["q_codes"][i, h], r["q_scales"][i, h],
