@@ -85,6 +85,25 @@ typedef enum {
                                   after the product, before masking.  Agrees with the seeded
                                   placements up to FP32 rounding order (not bit-identical).
                                   Exclusive with MPFA_SEED_INIT.                          */
+#define MPFA_PV_BF16      64u  /* quantize + prefill: precision assignment NVFP4(QK) + BF16(PV)
+                                  of the characterization in Sec. 3.1 / Fig. 3a: the
+                                  quantizer also stores V in BF16 in v_aux (bf16
+                                  [P][H_kv][128][64], channel-major like v_codes), and the
+                                  prefill rounds P to BF16 (no scale) and runs PV on the
+                                  BF16 MFMA over v_aux.  Not with MPFA_MXFP4,
+                                  MPFA_SEED_INIT or MPFA_SEED_ELEMWISE; decode: unsupported. */
+#define MPFA_PV_NVFP4    128u  /* quantize + prefill: NVFP4(QK) + NVFP4(PV), the other arm of
+                                  Fig. 3a: the quantizer stores V as NVFP4 in 16-key groups
+                                  per channel in v_aux (a code plane u8 [P][H_kv][128][32],
+                                  key 2i in the low nibble of byte i, then a scale plane u8
+                                  [P][H_kv][128][4] of E4M3 group scales, tensor scale 1);
+                                  the prefill quantizes P' = 2688 P per 16 keys with dynamic
+                                  E4M3 scales (amax / 6) and runs PV on FP16 MFMA over the
+                                  exactly dequantized operands.  Quantizer precondition: the
+                                  call is a fresh prefill (token i of a sequence at slot
+                                  i % 64 of its i / 64-th page); each page it touches is
+                                  written whole, absent slots as zero.  Same exclusions as
+                                  MPFA_PV_BF16.                                             */
 #define MPFA_MXFP4        16u  /* Q/K in MXFP4 instead of NVFP4 (quantize, prefill, decode):
                                   one E8M0 scale per 32 channels (scale bytes 0..3 of the
                                   8-byte scale row; bytes 4..7 zero), tensor scales 1, and
@@ -124,7 +143,8 @@ typedef struct {
     int32_t max_seqlen;       /* host: max tokens of one sequence in this call   */
     int32_t h_q, h_kv;        /* heads; h_q % h_kv == 0, h_q <= MPFA_MAX_HEADS   */
     int32_t head_dim;         /* must be 128                                     */
-    uint32_t flags;           /* MPFA_SMOOTH | MPFA_COMPUTE_STATS | MPFA_TSCALE_UNIT | MPFA_MXFP4 */
+    uint32_t flags;           /* MPFA_SMOOTH | MPFA_COMPUTE_STATS | MPFA_TSCALE_UNIT | MPFA_MXFP4
+                                 | MPFA_PV_BF16 or MPFA_PV_NVFP4 */
     int64_t num_pages;        /* cache capacity in pages (slot_mapping < 64 * num_pages) */
     const int32_t* cu_seqlens;   /* [batch+1]                                    */
     const void* q;               /* bf16 [T][h_q][128]                           */
@@ -141,6 +161,8 @@ typedef struct {
     uint8_t* k_scales;
     uint8_t* v_codes;
     void* ds;                    /* bf16 cache; may be NULL without MPFA_SMOOTH  */
+    void* v_aux;                 /* with MPFA_PV_BF16 / MPFA_PV_NVFP4 (see there); else
+                                    ignored (may be NULL)                          */
 } mpfa_quant_args;
 
 mpfa_status mpfa_quantize_qk(const mpfa_quant_args* args, mpfa_stream_t stream);
@@ -167,7 +189,8 @@ typedef struct {
     int32_t batch, h_q, h_kv, head_dim;
     int32_t max_seqlen_q;     /* host: max query tokens of one sequence          */
     int32_t max_pages;        /* page_table row length                           */
-    uint32_t flags;           /* MPFA_SMOOTH, MPFA_SEED_INIT or MPFA_SEED_ELEMWISE, MPFA_MXFP4 */
+    uint32_t flags;           /* MPFA_SMOOTH, MPFA_SEED_INIT or MPFA_SEED_ELEMWISE, MPFA_MXFP4,
+                                 MPFA_PV_BF16 or MPFA_PV_NVFP4                   */
     const int32_t* cu_seqlens_q; /* [batch+1] query tokens                       */
     const int32_t* q_start;   /* [batch] absolute position of query 0            */
     const int32_t* kv_len;    /* [batch] keys in the cache (>= q_start + n_q)    */
@@ -181,6 +204,9 @@ typedef struct {
     const void* ds;           /* bf16 side cache (MPFA_SMOOTH)                   */
     const float* k_tscale;    /* [batch][h_kv]                                   */
     void* out;                /* bf16 [T][h_q][128]                              */
+    const void* v_aux;        /* with MPFA_PV_BF16 / MPFA_PV_NVFP4; else ignored */
+    int64_t num_pages;        /* cache capacity in pages (plane offset of an NVFP4
+                                 v_aux); read only with MPFA_PV_NVFP4            */
 } mpfa_prefill_args;
 
 mpfa_status mpfa_prefill(const mpfa_prefill_args* args, mpfa_stream_t stream);

@@ -14,6 +14,7 @@ LIB_PATH = os.path.join(PKG_DIR, "libmpfa.so")
 
 MPFA_OK, MPFA_ERR_INVALID, MPFA_ERR_UNSUPPORTED, MPFA_ERR_WORKSPACE, MPFA_ERR_HIP = range(5)
 SMOOTH, COMPUTE_STATS, TSCALE_UNIT, SEED_INIT, MXFP4, SEED_ELEMWISE = 1, 2, 4, 8, 16, 32
+PV_BF16, PV_NVFP4 = 64, 128
 HEAD_DIM, PAGE, TILE = 128, 64, 128
 
 EXPORTED = ("mpfa_quantize_qk", "mpfa_prefill", "mpfa_decode_workspace_size",
@@ -35,7 +36,8 @@ class QuantArgs(C.Structure):
                 ("v", C.c_void_p), ("slot_mapping", C.c_void_p), ("q_mean", C.c_void_p),
                 ("k_mean", C.c_void_p), ("k_tscale", C.c_void_p), ("q_codes", C.c_void_p),
                 ("q_scales", C.c_void_p), ("q_tscale", C.c_void_p), ("k_codes", C.c_void_p),
-                ("k_scales", C.c_void_p), ("v_codes", C.c_void_p), ("ds", C.c_void_p)]
+                ("k_scales", C.c_void_p), ("v_codes", C.c_void_p), ("ds", C.c_void_p),
+                ("v_aux", C.c_void_p)]
 
 
 class PrefillArgs(C.Structure):
@@ -45,7 +47,8 @@ class PrefillArgs(C.Structure):
                 ("kv_len", C.c_void_p), ("page_table", C.c_void_p), ("q_codes", C.c_void_p),
                 ("q_scales", C.c_void_p), ("q_tscale", C.c_void_p), ("k_codes", C.c_void_p),
                 ("k_scales", C.c_void_p), ("v_codes", C.c_void_p), ("ds", C.c_void_p),
-                ("k_tscale", C.c_void_p), ("out", C.c_void_p)]
+                ("k_tscale", C.c_void_p), ("out", C.c_void_p), ("v_aux", C.c_void_p),
+                ("num_pages", C.c_int64)]
 
 
 class DecodeArgs(C.Structure):
@@ -112,7 +115,8 @@ def _check(rc: int, what: str):
 class PagedCache:
     """Device buffers of the paged NVFP4/FP8 KV cache and the Delta_S side cache."""
 
-    def __init__(self, num_pages: int, h_q: int, h_kv: int, device="cuda", smooth=True):
+    def __init__(self, num_pages: int, h_q: int, h_kv: int, device="cuda", smooth=True, pv=0):
+        """pv: 0, PV_BF16 or PV_NVFP4 (adds the V copy of that precision, v_aux)."""
         import torch
         self.num_pages, self.h_q, self.h_kv = num_pages, h_q, h_kv
         u8 = dict(dtype=torch.uint8, device=device)
@@ -121,6 +125,12 @@ class PagedCache:
         self.v_codes = torch.zeros((num_pages, h_kv, HEAD_DIM, PAGE), **u8)
         self.ds = torch.zeros((num_pages, h_q, PAGE), dtype=torch.bfloat16, device=device) \
             if smooth else None
+        self.v_aux = None
+        if pv == PV_BF16:
+            self.v_aux = torch.zeros((num_pages, h_kv, HEAD_DIM, PAGE), dtype=torch.bfloat16,
+                                     device=device)
+        elif pv == PV_NVFP4:   # code plane [P][H][128][32], then scale plane [P][H][128][4]
+            self.v_aux = torch.zeros(num_pages * h_kv * HEAD_DIM * 36, **u8)
 
 
 class SeqStats:
@@ -154,7 +164,8 @@ def quantize_qk(q, k, v, cu_seqlens, slot_mapping, cache: PagedCache, stats: Seq
                   k_mean=_ptr(stats.k_mean), k_tscale=_ptr(stats.k_tscale),
                   q_codes=_ptr(qout.codes), q_scales=_ptr(qout.scales),
                   q_tscale=_ptr(qout.tscale), k_codes=_ptr(cache.k_codes),
-                  k_scales=_ptr(cache.k_scales), v_codes=_ptr(cache.v_codes), ds=_ptr(cache.ds))
+                  k_scales=_ptr(cache.k_scales), v_codes=_ptr(cache.v_codes), ds=_ptr(cache.ds),
+                  v_aux=_ptr(cache.v_aux))
     _check(lib().mpfa_quantize_qk(C.byref(a), _stream(stream)), "mpfa_quantize_qk")
 
 
@@ -168,7 +179,8 @@ def prefill(qq: QuantQ, cache: PagedCache, stats: SeqStats, cu_seqlens_q, q_star
                     q_scales=_ptr(qq.scales), q_tscale=_ptr(qq.tscale),
                     k_codes=_ptr(cache.k_codes), k_scales=_ptr(cache.k_scales),
                     v_codes=_ptr(cache.v_codes), ds=_ptr(cache.ds),
-                    k_tscale=_ptr(stats.k_tscale), out=_ptr(out))
+                    k_tscale=_ptr(stats.k_tscale), out=_ptr(out), v_aux=_ptr(cache.v_aux),
+                    num_pages=cache.num_pages)
     _check(lib().mpfa_prefill(C.byref(a), _stream(stream)), "mpfa_prefill")
 
 

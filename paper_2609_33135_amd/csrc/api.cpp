@@ -44,8 +44,12 @@ mpfa_status mpfa_quantize_qk(const mpfa_quant_args* a, mpfa_stream_t stream) {
   if (a->batch < 1 || a->total_tokens < 0 || a->max_seqlen < 0 || a->num_pages < 1)
     return MPFA_ERR_INVALID;
   if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
-  if (a->flags & ~(MPFA_SMOOTH | MPFA_COMPUTE_STATS | MPFA_TSCALE_UNIT | MPFA_MXFP4))
+  if (a->flags & ~(MPFA_SMOOTH | MPFA_COMPUTE_STATS | MPFA_TSCALE_UNIT | MPFA_MXFP4 | MPFA_PV_BF16 |
+                   MPFA_PV_NVFP4))
     return MPFA_ERR_INVALID;
+  const uint32_t pvq = a->flags & (MPFA_PV_BF16 | MPFA_PV_NVFP4);
+  if (pvq == (MPFA_PV_BF16 | MPFA_PV_NVFP4) || (pvq && !a->v_aux)) return MPFA_ERR_INVALID;
+  if (pvq && (a->flags & MPFA_MXFP4)) return MPFA_ERR_UNSUPPORTED;
   const bool smooth = a->flags & MPFA_SMOOTH;
   if (!a->cu_seqlens || !a->q || !a->k || !a->v || !a->slot_mapping || !a->q_mean || !a->k_mean ||
       !a->k_tscale || !a->q_codes || !a->q_scales || !a->q_tscale || !a->k_codes || !a->k_scales ||
@@ -81,6 +85,9 @@ mpfa_status mpfa_quantize_qk(const mpfa_quant_args* a, mpfa_stream_t stream) {
   p.k_scales = a->k_scales;
   p.v_codes = a->v_codes;
   p.ds = static_cast<uint16_t*>(a->ds);
+  p.pv = (a->flags & MPFA_PV_BF16) ? 1 : (a->flags & MPFA_PV_NVFP4) ? 2 : 0;
+  p.v_aux = static_cast<uint8_t*>(a->v_aux);
+  p.num_pages = a->num_pages;
   return mpfa::launch_quantize(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
                                                                                         : MPFA_ERR_HIP;
 }
@@ -90,8 +97,14 @@ mpfa_status mpfa_prefill(const mpfa_prefill_args* a, mpfa_stream_t stream) {
   if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
   if (a->batch < 1 || a->max_seqlen_q < 0 || a->max_pages < 1) return MPFA_ERR_INVALID;
   if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
-  if (a->flags & ~(MPFA_SMOOTH | MPFA_SEED_INIT | MPFA_SEED_ELEMWISE | MPFA_MXFP4)) return MPFA_ERR_INVALID;
+  if (a->flags & ~(MPFA_SMOOTH | MPFA_SEED_INIT | MPFA_SEED_ELEMWISE | MPFA_MXFP4 | MPFA_PV_BF16 |
+                   MPFA_PV_NVFP4))
+    return MPFA_ERR_INVALID;
   if ((a->flags & MPFA_SEED_INIT) && (a->flags & MPFA_SEED_ELEMWISE)) return MPFA_ERR_INVALID;
+  const uint32_t pvp = a->flags & (MPFA_PV_BF16 | MPFA_PV_NVFP4);
+  if (pvp == (MPFA_PV_BF16 | MPFA_PV_NVFP4) || (pvp && !a->v_aux)) return MPFA_ERR_INVALID;
+  if ((pvp & MPFA_PV_NVFP4) && a->num_pages < 1) return MPFA_ERR_INVALID;
+  if (pvp && (a->flags & (MPFA_MXFP4 | MPFA_SEED_INIT | MPFA_SEED_ELEMWISE))) return MPFA_ERR_UNSUPPORTED;
   const bool smooth = a->flags & MPFA_SMOOTH;
   if (!a->cu_seqlens_q || !a->q_start || !a->kv_len || !a->page_table || !a->q_codes ||
       !a->q_scales || !a->q_tscale || !a->k_codes || !a->k_scales || !a->v_codes ||
@@ -109,6 +122,9 @@ mpfa_status mpfa_prefill(const mpfa_prefill_args* a, mpfa_stream_t stream) {
   p.smooth = smooth;
   p.seed_init = (a->flags & MPFA_SEED_INIT) != 0;
   p.seed_elem = (a->flags & MPFA_SEED_ELEMWISE) != 0;
+  p.pv = (a->flags & MPFA_PV_BF16) ? 1 : (a->flags & MPFA_PV_NVFP4) ? 2 : 0;
+  p.v_aux = static_cast<const uint8_t*>(a->v_aux);
+  p.num_pages = a->num_pages;
   p.mx = (a->flags & MPFA_MXFP4) != 0;
   p.xcd_remap = (a->h_kv % 8) == 0;
   p.lam = kLambda;
@@ -164,6 +180,7 @@ mpfa_status mpfa_decode_paged(const mpfa_decode_args* a, void* workspace, size_t
     return MPFA_ERR_INVALID;
   if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
   if (a->h_q / a->h_kv > kMaxDecodeGroup) return MPFA_ERR_UNSUPPORTED;
+  if (a->flags & (MPFA_PV_BF16 | MPFA_PV_NVFP4)) return MPFA_ERR_UNSUPPORTED;
   if (a->flags & ~(MPFA_SMOOTH | MPFA_MXFP4)) return MPFA_ERR_INVALID;
   const bool smooth = a->flags & MPFA_SMOOTH;
   if (!a->kv_len || !a->page_table || !a->q_codes || !a->q_scales || !a->q_tscale ||

@@ -90,6 +90,41 @@ __device__ __forceinline__ float tensor_scale(float amax) {
   return __builtin_ldexpf(1.0f, k);
 }
 
+// Element conversions through the gfx950 converters.  Over every finite FP32
+// input these give the same bytes as e2m1_rne_sat / e4m3_rne_sat (checked
+// exhaustively on the device): v_cvt_scalef32_pk_fp4_f32 rounds to nearest
+// even and saturates at 6 after dividing by the power of two in its scale
+// operand; v_cvt_pk_fp8_f32 rounds to nearest even, and clamping to +-448
+// first makes it saturate as the E4M3 encoder does.
+__device__ __forceinline__ uint32_t fp4_pair(uint32_t w, float a, float b, float pow2, int sel) {
+  switch (sel) {   // the byte selector must be an immediate
+    case 0: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 0);
+    case 1: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 1);
+    case 2: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 2);
+    default: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 3);
+  }
+}
+__device__ __forceinline__ uint32_t fp8_sat_pair(uint32_t w, float a, float b, bool hi) {
+  a = fminf(fmaxf(a, -448.0f), 448.0f);
+  b = fminf(fmaxf(b, -448.0f), 448.0f);
+  return hi ? (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)w, true)
+            : (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)w, false);
+}
+
+// RN(x / s) from r = RN(1 / s): one product and one residual correction.  For
+// divisors s = 2^k * (E4M3 value) this equals the correctly rounded quotient
+// for every FP32 x whose quotient is at least 2^-100 in magnitude (checked
+// exhaustively on the device over all x and all 126 positive E4M3 values);
+// smaller quotients round to the zero E2M1 code either way.  The sign is
+// restored for x = -0 (the correction would return +0).
+__device__ __forceinline__ float div_by_scale(float x, float s, float r) {
+  const float q0 = x * r;
+  const float e = __builtin_fmaf(-s, q0, x);
+  return __builtin_copysignf(__builtin_fmaf(e, r, q0), x);
+}
+
+constexpr float kRcp6 = 0x1.555556p-3f;   // RN(1/6)
+
 // ---------------------------------------------------------------------------
 // Exact NVFP4 -> FP16 dequantization.
 // An E4M3 scale s = 2^E * M splits into a power of two (E in [-6, 8]) and a

@@ -29,6 +29,9 @@ struct QuantParams {
   uint8_t* k_scales;
   uint8_t* v_codes;
   uint16_t* ds;
+  int pv;           // 0: FP8 V only; 1: also BF16 V in v_aux; 2: also NVFP4 V in v_aux
+  uint8_t* v_aux;
+  int64_t num_pages;
 };
 
 struct PrefillParams {
@@ -53,6 +56,9 @@ struct PrefillParams {
   const uint16_t* ds;
   const float* k_tscale;
   uint16_t* out;
+  int pv;           // 0: FP8 P and V; 1: BF16 P and V (v_aux); 2: NVFP4 P and V (v_aux)
+  const uint8_t* v_aux;
+  int64_t num_pages;
 };
 
 struct DecodeParams {

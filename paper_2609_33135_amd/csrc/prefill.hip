@@ -30,12 +30,23 @@ constexpr int kNB = 2;                       // 16-row query blocks per wave
 constexpr int kQRows = kWaves * kNB * 16;    // 256 query rows per workgroup
 constexpr int kThreads = kWaves * 64;
 
-struct PrefillSmem {
+// Precision of the PV product: the method's FP8 (P * 448 and V in E4M3), or
+// the two other assignments compared in Sec. 3.1 / Fig. 3a, BF16 P and V, and
+// NVFP4 P (2688 P quantized per 16 keys with dynamic E4M3 scales) with NVFP4 V
+// (16-key groups per channel, tensor scale 1), both on FP16 / BF16 MFMA after
+// exact dequantization.
+enum PvMode { kPvFp8 = 0, kPvBf16 = 1, kPvNvfp4 = 2 };
+
+template <int PV>
+struct PrefillSmemT {
   // NVFP4: FP16 [key][128], 16-byte chunks XOR-swizzled per key.  MXFP4: raw
   // codes [key][64] (chunks swizzled by mx_swz) in the first 8 KB, then the
   // E8M0 scales transposed to [MFMA row][32-channel block][16-key block].
   uint8_t k[kTile * 256];
-  uint8_t v[kD * kTile];    // FP8 [channel][key], 16-byte chunks XOR-swizzled per channel
+  // FP8: [channel][key] bytes, 16-byte chunks XOR-swizzled per channel (v_swz).
+  // BF16 / NVFP4: [channel][key] BF16 or exact FP16, 256-byte rows of 16
+  // chunks, chunk c of channel d stored at position c ^ (d & 15).
+  uint8_t v[kD * kTile * (PV == kPvFp8 ? 1 : 2)];
   uint16_t ds[kTile];       // BF16 seed values in accumulator units
 };
 
@@ -59,15 +70,20 @@ __device__ __forceinline__ u32x4 zero_tail(u32x4 w, int nvalid) {
 // Raw bytes of one KV tile held in registers between the global load and the
 // LDS store (software pipelining: the next tile is fetched while the current
 // one is computed).
+template <int PV>
 struct TileRegs {
   u32x4 kc;        // 16 NVFP4 code bytes: key t/4, channels 32*(t%4) .. +31
   uint32_t ksc;    // their two E4M3 group scales
-  u32x4 v0, v1;    // 32 FP8 bytes: channel t/4, keys 32*(t%4) .. +31 of the tile
+  // channel t/4, keys 32*(t%4) .. +31 of the tile: 32 FP8 bytes, 32 BF16
+  // values, or 32 E2M1 codes (16 bytes)
+  static constexpr int kVWords = PV == kPvFp8 ? 2 : (PV == kPvBf16 ? 4 : 1);
+  u32x4 v[kVWords];
+  uint32_t vsc;    // NVFP4 V: the two E4M3 scales of those keys
   uint32_t ds;     // BF16 Delta_S of key t (threads 0..127)
 };
 
-template <bool MX>
-__device__ __forceinline__ void fetch_tile(TileRegs& r, const PrefillParams& p, const int32_t* pt,
+template <bool MX, int PV>
+__device__ __forceinline__ void fetch_tile(TileRegs<PV>& r, const PrefillParams& p, const int32_t* pt,
                                            int hk, int h, int j, int kvl) {
   const int t = threadIdx.x;
   // the two pages of tile j: uniform across the workgroup (scalar loads)
@@ -89,16 +105,33 @@ __device__ __forceinline__ void fetch_tile(TileRegs& r, const PrefillParams& p, 
   {
     const int d = t >> 2, part = t & 3;
     const int kbase = j * kTile + part * 32;
-    r.v0 = (u32x4){0u, 0u, 0u, 0u};
-    r.v1 = (u32x4){0u, 0u, 0u, 0u};
+    const int64_t crow = ((part < 2 ? pg0 : pg1) * p.h_kv + hk) * kD + d;   // channel row of the page
+#pragma unroll
+    for (int i = 0; i < TileRegs<PV>::kVWords; ++i) r.v[i] = (u32x4){0u, 0u, 0u, 0u};
+    r.vsc = 0;
     if (kbase < kvl) {
-      const uint8_t* src = p.v_codes + (((part < 2 ? pg0 : pg1) * p.h_kv + hk) * kD + d) * kPage +
-                           (kbase & 63);
-      r.v0 = *reinterpret_cast<const u32x4*>(src);
-      r.v1 = *reinterpret_cast<const u32x4*>(src + 16);
-      if (kbase + 32 > kvl) {
-        r.v0 = zero_tail(r.v0, kvl - kbase);
-        r.v1 = zero_tail(r.v1, kvl - kbase - 16);
+      if (PV == kPvFp8) {
+        const uint8_t* src = p.v_codes + crow * kPage + (kbase & 63);
+        r.v[0] = *reinterpret_cast<const u32x4*>(src);
+        r.v[1 % TileRegs<PV>::kVWords] = *reinterpret_cast<const u32x4*>(src + 16);
+        if (kbase + 32 > kvl) {
+          r.v[0] = zero_tail(r.v[0], kvl - kbase);
+          r.v[1 % TileRegs<PV>::kVWords] = zero_tail(r.v[1 % TileRegs<PV>::kVWords], kvl - kbase - 16);
+        }
+      } else if (PV == kPvBf16) {
+        const uint8_t* src = p.v_aux + (crow * kPage + (kbase & 63)) * 2;
+#pragma unroll
+        for (int i = 0; i < TileRegs<PV>::kVWords; ++i) {
+          r.v[i] = *reinterpret_cast<const u32x4*>(src + 16 * i);
+          // keys past kv_len: zero (slots not written may hold any bits)
+          if (kbase + 32 > kvl) r.v[i] = zero_tail(r.v[i], 2 * (kvl - kbase) - 16 * i);
+        }
+      } else {
+        // NVFP4 dequantizes to finite values whatever the bytes, and P is 0 on
+        // keys past kv_len: nothing to clear
+        r.v[0] = *reinterpret_cast<const u32x4*>(p.v_aux + crow * 32 + (kbase & 63) / 2);
+        r.vsc = *reinterpret_cast<const uint16_t*>(p.v_aux + p.num_pages * p.h_kv * kD * 32 + crow * 4 +
+                                                   (kbase & 63) / 16);
       }
     }
   }
@@ -110,8 +143,8 @@ __device__ __forceinline__ void fetch_tile(TileRegs& r, const PrefillParams& p, 
   }
 }
 
-template <bool MX>
-__device__ __forceinline__ void store_tile(PrefillSmem& sm, const TileRegs& r, float seed_scale) {
+template <bool MX, int PV>
+__device__ __forceinline__ void store_tile(PrefillSmemT<PV>& sm, const TileRegs<PV>& r, float seed_scale) {
   const int t = threadIdx.x;
   if (MX) {
     const int key = t >> 2, qt = t & 3;
@@ -131,10 +164,25 @@ __device__ __forceinline__ void store_tile(PrefillSmem& sm, const TileRegs& r, f
   }
   {
     const int d = t >> 2, part = t & 3;
-    uint8_t* rowp = sm.v + d * kTile;
-    const int sw = v_swz(d);
-    *reinterpret_cast<u32x4*>(rowp + (((2 * part) ^ sw) << 4)) = r.v0;
-    *reinterpret_cast<u32x4*>(rowp + (((2 * part + 1) ^ sw) << 4)) = r.v1;
+    if (PV == kPvFp8) {
+      uint8_t* rowp = sm.v + d * kTile;
+      const int sw = v_swz(d);
+      *reinterpret_cast<u32x4*>(rowp + (((2 * part) ^ sw) << 4)) = r.v[0];
+      *reinterpret_cast<u32x4*>(rowp + (((2 * part + 1) ^ sw) << 4)) = r.v[1 % TileRegs<PV>::kVWords];
+    } else {
+      uint8_t* rowp = sm.v + d * (kTile * 2);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        u32x4 w;
+        if (PV == kPvBf16) {
+          w = r.v[i % TileRegs<PV>::kVWords];
+        } else {   // 8 codes of keys 32 part + 8i .. +7, the scale of their 16-key group
+          const f16x8 hv = dequant8(r.v[0][i], split_e4m3((r.vsc >> (8 * (i >> 1))) & 0xFFu));
+          w = __builtin_bit_cast(u32x4, hv);
+        }
+        *reinterpret_cast<u32x4*>(rowp + (((4 * part + i) ^ (d & 15)) << 4)) = w;
+      }
+    }
   }
   // exact: a BF16 value times a power of two stays a BF16 value
   if (t < kTile) sm.ds[t] = bf16_rne(bf16_to_f32((uint16_t)r.ds) * seed_scale);
@@ -155,9 +203,9 @@ __device__ __forceinline__ void store_tile(PrefillSmem& sm, const TileRegs& r, f
 //             values up to the FP32 rounding order.
 enum SeedMode { kSeedNone = 0, kSeedMfma = 1, kSeedInit = 2, kSeedElem = 3 };
 
-template <int SEED, bool MX>
+template <int SEED, bool MX, int PV>
 __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
-  __shared__ __attribute__((aligned(16))) PrefillSmem smem[2];
+  __shared__ __attribute__((aligned(16))) PrefillSmemT<PV> smem[2];
 
   // ---- work item: largest query tiles first (longest-processing-time order)
   int b, h, rank;
@@ -248,15 +296,15 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
 
   const int32_t* pt = p.page_table + (int64_t)b * p.max_pages;
   {
-    TileRegs r0r;
-    fetch_tile<MX>(r0r, p, pt, hk, h, j_hi, kvl);
-    store_tile<MX>(smem[j_hi & 1], r0r, seed_scale);
+    TileRegs<PV> r0r;
+    fetch_tile<MX, PV>(r0r, p, pt, hk, h, j_hi, kvl);
+    store_tile<MX, PV>(smem[j_hi & 1], r0r, seed_scale);
   }
   __syncthreads();
   for (int j = j_hi; j >= 0; --j) {
-    TileRegs nxt;
-    if (j > 0) fetch_tile<MX>(nxt, p, pt, hk, h, j - 1, kvl);
-    const PrefillSmem& sm = smem[j & 1];
+    TileRegs<PV> nxt;
+    if (j > 0) fetch_tile<MX, PV>(nxt, p, pt, hk, h, j - 1, kvl);
+    const PrefillSmemT<PV>& sm = smem[j & 1];
     const int key0 = j * kTile;
     if (wave_active && key0 <= wpos_max) {
       const bool need_mask = key0 + kTile - 1 > wpos_min;
@@ -324,7 +372,12 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
             for (int i = 0; i < 4; ++i)
               if (key0 + 32 * g + 4 * mb + i > pos[nb]) s[mb][nb][i] = -INFINITY;
       }
+      // log2 of the fixed factor the P quantizer applies: 448 (FP8), 1 (BF16),
+      // 2688 = 6 * 448 (NVFP4: the largest P, 1, maps to the top E2M1 code
+      // under the largest E4M3 scale)
+      constexpr float kLog2PScale = PV == kPvFp8 ? kLog2_448 : (PV == kPvBf16 ? 0.0f : 11.392317422778760f);
       i32x8 pb[kNB];
+      f16x8 ph[kNB][4];   // BF16 (bit pattern) or dequantized NVFP4 P, keys 32g + 8kk .. +7
       float alpha[kNB];
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb) {
@@ -337,8 +390,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
         const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
         alpha[nb] = (m[nb] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m[nb] - muse) * lam2);
         m[nb] = mnew;
-        const float bias = __builtin_fmaf(-muse, lam2, kLog2_448);
+        const float bias = __builtin_fmaf(-muse, lam2, kLog2PScale);
         float ps = 0.0f;
+        float ev[8][4];
 #pragma unroll
         for (int mb = 0; mb < 8; ++mb) {
           float e[4];
@@ -346,9 +400,54 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
           for (int i = 0; i < 4; ++i)
             e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][nb][i], lam2, bias));
           ps += (e[0] + e[1]) + (e[2] + e[3]);
-          pb[nb][mb] = (int)pack_fp8x4(e[0], e[1], e[2], e[3]);
+          if (PV == kPvFp8) {
+            pb[nb][mb] = (int)pack_fp8x4(e[0], e[1], e[2], e[3]);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) ev[mb][i] = e[i];
+          }
         }
         l[nb] = alpha[nb] * l[nb] + ps;
+        if (PV == kPvBf16) {
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk) {
+            bf16x8 b;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              b[i] = (__bf16)ev[2 * kk][i];
+              b[4 + i] = (__bf16)ev[2 * kk + 1][i];
+            }
+            ph[nb][kk] = __builtin_bit_cast(f16x8, b);
+          }
+        } else if (PV == kPvNvfp4) {
+          // the lane's 32 keys are two 16-key groups: keys 32g .. +15 (mb 0..3)
+          // and 32g + 16 .. +31 (mb 4..7); scale E4M3(amax / 6), codes E2M1(P'/scale)
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            float amax = 0.0f;
+#pragma unroll
+            for (int mb = 4 * half; mb < 4 * half + 4; ++mb)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) amax = fmaxf(amax, ev[mb][i]);
+            const uint32_t sc = fp8_sat_pair(0u, div_by_scale(amax, 6.0f, kRcp6), 0.0f, false) & 0xFFu;
+            const float sd = e4m3_value(sc);
+            uint32_t cw[2] = {0u, 0u};
+            if (sd > 0.0f) {
+              const float r = __fdiv_rn(1.0f, sd);
+#pragma unroll
+              for (int w = 0; w < 2; ++w)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                  const int mb = 4 * half + 2 * w + (j >> 1), i0 = 2 * (j & 1);
+                  cw[w] = fp4_pair(cw[w], div_by_scale(ev[mb][i0], sd, r), div_by_scale(ev[mb][i0 + 1], sd, r),
+                                   1.0f, j);
+                }
+            }
+            const ScaleSplit sp = split_e4m3(sc);
+            ph[nb][2 * half] = dequant8(cw[0], sp);
+            ph[nb][2 * half + 1] = dequant8(cw[1], sp);
+          }
+        }
       }
       bool moved = false;
 #pragma unroll
@@ -359,20 +458,42 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
 #pragma unroll
           for (int nb = 0; nb < kNB; ++nb) o[db][nb] *= alpha[nb];
       }
+      if (PV == kPvFp8) {
 #pragma unroll
-      for (int db = 0; db < 8; ++db) {
-        const int d = 16 * db + lr;
-        const uint8_t* vr = sm.v + d * kTile;
-        const int sw = v_swz(d);
-        const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((2 * g) ^ sw) << 4));
-        const u32x4 vb = *reinterpret_cast<const u32x4*>(vr + (((2 * g + 1) ^ sw) << 4));
-        const i32x8 vop = {(int)va[0], (int)va[1], (int)va[2], (int)va[3],
-                           (int)vb[0], (int)vb[1], (int)vb[2], (int)vb[3]};
+        for (int db = 0; db < 8; ++db) {
+          const int d = 16 * db + lr;
+          const uint8_t* vr = sm.v + d * kTile;
+          const int sw = v_swz(d);
+          const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((2 * g) ^ sw) << 4));
+          const u32x4 vb = *reinterpret_cast<const u32x4*>(vr + (((2 * g + 1) ^ sw) << 4));
+          const i32x8 vop = {(int)va[0], (int)va[1], (int)va[2], (int)va[3],
+                             (int)vb[0], (int)vb[1], (int)vb[2], (int)vb[3]};
 #pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) o[db][nb] = mfma_fp8(vop, pb[nb], o[db][nb]);
+          for (int nb = 0; nb < kNB; ++nb) o[db][nb] = mfma_fp8(vop, pb[nb], o[db][nb]);
+        }
+      } else {
+        // four 32-key MFMAs per channel block: MFMA kk reduces keys 32g + 8kk .. +7
+        // of every lane group g, so A (V row chunk 4g + kk) and B (the lane's own
+        // P values) pair the same keys
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+          const uint8_t* vr = sm.v + (16 * db + lr) * (kTile * 2);
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk) {
+            const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((4 * g + kk) ^ lr) << 4));
+#pragma unroll
+            for (int nb = 0; nb < kNB; ++nb) {
+              if (PV == kPvBf16)
+                o[db][nb] = mfma_bf16(__builtin_bit_cast(bf16x8, va), __builtin_bit_cast(bf16x8, ph[nb][kk]),
+                                      o[db][nb]);
+              else
+                o[db][nb] = mfma_f16(__builtin_bit_cast(f16x8, va), ph[nb][kk], o[db][nb]);
+            }
+          }
+        }
       }
     }
-    if (j > 0) store_tile<MX>(smem[(j - 1) & 1], nxt, seed_scale);
+    if (j > 0) store_tile<MX, PV>(smem[(j - 1) & 1], nxt, seed_scale);
     __syncthreads();
   }
 
@@ -403,16 +524,22 @@ hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream) {
   const unsigned blocks = (unsigned)(p.n_qtiles * p.h_q * p.batch);
   if (blocks == 0) return hipSuccess;
   const dim3 grid(blocks), block(kThreads);
-  if (p.mx) {
-    if (!p.smooth) prefill_kernel<kSeedNone, true><<<grid, block, 0, stream>>>(p);
-    else if (p.seed_init) prefill_kernel<kSeedInit, true><<<grid, block, 0, stream>>>(p);
-    else if (p.seed_elem) prefill_kernel<kSeedElem, true><<<grid, block, 0, stream>>>(p);
-    else prefill_kernel<kSeedMfma, true><<<grid, block, 0, stream>>>(p);
+  if (p.pv == kPvBf16) {
+    if (!p.smooth) prefill_kernel<kSeedNone, false, kPvBf16><<<grid, block, 0, stream>>>(p);
+    else prefill_kernel<kSeedMfma, false, kPvBf16><<<grid, block, 0, stream>>>(p);
+  } else if (p.pv == kPvNvfp4) {
+    if (!p.smooth) prefill_kernel<kSeedNone, false, kPvNvfp4><<<grid, block, 0, stream>>>(p);
+    else prefill_kernel<kSeedMfma, false, kPvNvfp4><<<grid, block, 0, stream>>>(p);
+  } else if (p.mx) {
+    if (!p.smooth) prefill_kernel<kSeedNone, true, kPvFp8><<<grid, block, 0, stream>>>(p);
+    else if (p.seed_init) prefill_kernel<kSeedInit, true, kPvFp8><<<grid, block, 0, stream>>>(p);
+    else if (p.seed_elem) prefill_kernel<kSeedElem, true, kPvFp8><<<grid, block, 0, stream>>>(p);
+    else prefill_kernel<kSeedMfma, true, kPvFp8><<<grid, block, 0, stream>>>(p);
   } else {
-    if (!p.smooth) prefill_kernel<kSeedNone, false><<<grid, block, 0, stream>>>(p);
-    else if (p.seed_init) prefill_kernel<kSeedInit, false><<<grid, block, 0, stream>>>(p);
-    else if (p.seed_elem) prefill_kernel<kSeedElem, false><<<grid, block, 0, stream>>>(p);
-    else prefill_kernel<kSeedMfma, false><<<grid, block, 0, stream>>>(p);
+    if (!p.smooth) prefill_kernel<kSeedNone, false, kPvFp8><<<grid, block, 0, stream>>>(p);
+    else if (p.seed_init) prefill_kernel<kSeedInit, false, kPvFp8><<<grid, block, 0, stream>>>(p);
+    else if (p.seed_elem) prefill_kernel<kSeedElem, false, kPvFp8><<<grid, block, 0, stream>>>(p);
+    else prefill_kernel<kSeedMfma, false, kPvFp8><<<grid, block, 0, stream>>>(p);
   }
   return hipGetLastError();
 }

@@ -210,44 +210,10 @@ __global__ __launch_bounds__(128) void stats_final_kernel(QuantParams p) {
   if (c == 0) write_tscale(p, b, hh, fmaxf(red[0], red[1]));
 }
 
-// Element conversions through the gfx950 converters.  Over every finite FP32
-// input these give the same bytes as e2m1_rne_sat / e4m3_rne_sat (checked
-// exhaustively on the device): v_cvt_scalef32_pk_fp4_f32 rounds to nearest
-// even and saturates at 6 after dividing by the power of two in its scale
-// operand; v_cvt_pk_fp8_f32 rounds to nearest even, and clamping to +-448
-// first makes it saturate as the E4M3 encoder does.
-__device__ __forceinline__ uint32_t fp4_pair(uint32_t w, float a, float b, float pow2, int sel) {
-  switch (sel) {   // the byte selector must be an immediate
-    case 0: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 0);
-    case 1: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 1);
-    case 2: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 2);
-    default: return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, a, b, pow2, 3);
-  }
-}
-__device__ __forceinline__ uint32_t fp8_sat_pair(uint32_t w, float a, float b, bool hi) {
-  a = fminf(fmaxf(a, -448.0f), 448.0f);
-  b = fminf(fmaxf(b, -448.0f), 448.0f);
-  return hi ? (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)w, true)
-            : (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)w, false);
-}
-
-// RN(x / s) from r = RN(1 / s): one product and one residual correction.  For
-// divisors s = 2^k * (E4M3 value) this equals the correctly rounded quotient
-// for every FP32 x whose quotient is at least 2^-100 in magnitude (checked
-// exhaustively on the device over all x and all 126 positive E4M3 values);
-// smaller quotients round to the zero E2M1 code either way.  The sign is
-// restored for x = -0 (the correction would return +0).
-__device__ __forceinline__ float div_by_scale(float x, float s, float r) {
-  const float q0 = x * r;
-  const float e = __builtin_fmaf(-s, q0, x);
-  return __builtin_copysignf(__builtin_fmaf(e, r, q0), x);
-}
-
 // NVFP4 quantization of one 16-channel group held as 16 centered FP32 values:
 // returns 8 code bytes (as a 64-bit word, low nibble first) and the scale byte.
 // rcp_sd[c] = RN(1 / e4m3_value(c)) for the positive E4M3 codes; with a
 // power-of-two t, RN(1 / (t * sd)) = rcp_sd / t and RN(1 / (6 t)) = RN(1/6) / t.
-constexpr float kRcp6 = 0x1.555556p-3f;   // RN(1/6)
 
 __device__ __forceinline__ uint64_t nvfp4_group(const float* xc, float t, const float* rcp_sd,
                                                 uint32_t* scale_code) {
@@ -385,7 +351,7 @@ __device__ __forceinline__ void quant_rows(const QuantParams& p, const uint16_t*
 
 template <bool MX>
 __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
-  __shared__ int page_run;   // 1: the chunk's 64 tokens are slots 0..63 of one page, in order
+  __shared__ int page_start;   // 1: the chunk's tokens are slots 0, 1, ... of one page, in order
   __shared__ float rcp_sd[128];
   extern __shared__ __attribute__((aligned(16))) uint8_t sm_mean[];   // [h_q + h_kv][kMeanStride]
   const int b = blockIdx.y;
@@ -398,13 +364,10 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
   const int tid = threadIdx.x;
 
   if (tid < 64) {
-    bool ok = cnt == kChunk;
-    if (ok) {
-      const int64_t s0 = p.slot_mapping[tok0];
-      ok = (s0 % kPage == 0) && p.slot_mapping[tok0 + tid] == s0 + tid;
-    }
+    const int64_t s0 = p.slot_mapping[tok0];
+    const bool ok = (s0 % kPage == 0) && (tid >= cnt || p.slot_mapping[tok0 + tid] == s0 + tid);
     const bool all = __builtin_amdgcn_ballot_w64(!ok) == 0;
-    if (tid == 0) page_run = all ? 1 : 0;
+    if (tid == 0) page_start = all ? 1 : 0;
   }
   if (!MX && tid < 128) rcp_sd[tid] = (tid & 0x7F) && tid < 0x7F ? __fdiv_rn(1.0f, e4m3_value(tid)) : 0.0f;
   // the sequence's Q and K means (zero rows without smoothing)
@@ -429,41 +392,78 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
                  true, p.k_codes, p.k_scales, rcp_sd);
   __syncthreads();
 
-  // V -> E4M3, channel-major page rows
-  if (page_run) {
+  // V -> E4M3, channel-major page rows (plus the characterization copies in
+  // v_aux: BF16 rows, or NVFP4 16-key groups along each channel row)
+  const bool page_run = page_start && cnt == kChunk;   // whole page rows can be written
+  if (page_run || (p.pv == 2 && page_start)) {
     const int64_t page = p.slot_mapping[tok0] / kPage;
+    const int64_t aux_scales = p.num_pages * p.h_kv * kD * 32;   // NVFP4 scale plane offset
     for (int u = tid; u < p.h_kv * (kD / 2); u += blockDim.x) {
       const int h = u / (kD / 2), cp = u % (kD / 2);
       const uint32_t* src = reinterpret_cast<const uint32_t*>(p.v + (tok0 * p.h_kv + h) * kD) + cp;
       const int64_t tstride = (int64_t)p.h_kv * (kD / 2);
-      uint8_t* dst = p.v_codes + ((page * p.h_kv + h) * kD + 2 * cp) * kPage;
+      const int64_t crow = (page * p.h_kv + h) * kD + 2 * cp;   // channel row 2cp; 2cp+1 follows
+      uint8_t* dst = p.v_codes + crow * kPage;
       // 16 tokens at a time: 16 bytes of each of the two channel rows
       for (int qq = 0; qq < kPage; qq += 16) {
         uint32_t w[16];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) w[j] = src[(int64_t)(qq + j) * tstride];
-        u32x4 r0, r1;   // bytes of channels 2cp and 2cp+1
+        for (int j = 0; j < 16; ++j) w[j] = qq + j < cnt ? src[(int64_t)(qq + j) * tstride] : 0u;
+        if (page_run) {
+          u32x4 r0, r1;   // bytes of channels 2cp and 2cp+1
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t* wq = w + 4 * q;
-          uint32_t a = fp8_sat_pair(0u, __uint_as_float(wq[0] << 16), __uint_as_float(wq[1] << 16), false);
-          a = fp8_sat_pair(a, __uint_as_float(wq[2] << 16), __uint_as_float(wq[3] << 16), true);
-          uint32_t c = fp8_sat_pair(0u, __uint_as_float(wq[0] & 0xFFFF0000u), __uint_as_float(wq[1] & 0xFFFF0000u), false);
-          c = fp8_sat_pair(c, __uint_as_float(wq[2] & 0xFFFF0000u), __uint_as_float(wq[3] & 0xFFFF0000u), true);
-          r0[q] = a;
-          r1[q] = c;
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t* wq = w + 4 * q;
+            uint32_t a = fp8_sat_pair(0u, __uint_as_float(wq[0] << 16), __uint_as_float(wq[1] << 16), false);
+            a = fp8_sat_pair(a, __uint_as_float(wq[2] << 16), __uint_as_float(wq[3] << 16), true);
+            uint32_t c = fp8_sat_pair(0u, __uint_as_float(wq[0] & 0xFFFF0000u), __uint_as_float(wq[1] & 0xFFFF0000u), false);
+            c = fp8_sat_pair(c, __uint_as_float(wq[2] & 0xFFFF0000u), __uint_as_float(wq[3] & 0xFFFF0000u), true);
+            r0[q] = a;
+            r1[q] = c;
+          }
+          *reinterpret_cast<u32x4*>(dst + qq) = r0;
+          *reinterpret_cast<u32x4*>(dst + kPage + qq) = r1;
+          if (p.pv == 1) {   // BF16 rows: 16 keys of each channel, 32 bytes
+            uint32_t b0[8], b1[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              b0[j] = (w[2 * j] & 0xFFFFu) | (w[2 * j + 1] << 16);
+              b1[j] = (w[2 * j] >> 16) | (w[2 * j + 1] & 0xFFFF0000u);
+            }
+            uint16_t* a16 = reinterpret_cast<uint16_t*>(p.v_aux) + crow * kPage + qq;
+            *reinterpret_cast<u32x4*>(a16) = (u32x4){b0[0], b0[1], b0[2], b0[3]};
+            *reinterpret_cast<u32x4*>(a16 + 8) = (u32x4){b0[4], b0[5], b0[6], b0[7]};
+            *reinterpret_cast<u32x4*>(a16 + kPage) = (u32x4){b1[0], b1[1], b1[2], b1[3]};
+            *reinterpret_cast<u32x4*>(a16 + kPage + 8) = (u32x4){b1[4], b1[5], b1[6], b1[7]};
+          }
         }
-        *reinterpret_cast<u32x4*>(dst + qq) = r0;
-        *reinterpret_cast<u32x4*>(dst + kPage + qq) = r1;
+        if (p.pv == 2) {   // one NVFP4 group per channel: these 16 keys (absent ones zero)
+          float x0[16], x1[16];
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            x0[j] = __uint_as_float(w[j] << 16);
+            x1[j] = __uint_as_float(w[j] & 0xFFFF0000u);
+          }
+          uint32_t sc0, sc1;
+          const uint64_t c0 = nvfp4_group(x0, 1.0f, rcp_sd, &sc0);
+          const uint64_t c1 = nvfp4_group(x1, 1.0f, rcp_sd, &sc1);
+          *reinterpret_cast<uint64_t*>(p.v_aux + crow * 32 + qq / 2) = c0;
+          *reinterpret_cast<uint64_t*>(p.v_aux + (crow + 1) * 32 + qq / 2) = c1;
+          p.v_aux[aux_scales + crow * 4 + qq / 16] = (uint8_t)sc0;
+          p.v_aux[aux_scales + (crow + 1) * 4 + qq / 16] = (uint8_t)sc1;
+        }
       }
     }
-  } else {
+  }
+  if (!page_run) {
     for (int u = tid; u < cnt * p.h_kv * kD; u += blockDim.x) {
       const int c = u % kD, ih = u / kD;
       const int h = ih % p.h_kv, i = ih / p.h_kv;
       const int64_t slot = p.slot_mapping[tok0 + i];
-      const float v = bf16_to_f32(p.v[(tok0 + i) * p.h_kv * kD + (int64_t)h * kD + c]);
-      p.v_codes[(((slot / kPage) * p.h_kv + h) * kD + c) * kPage + slot % kPage] = (uint8_t)e4m3_rne_sat(v);
+      const uint16_t vb = p.v[(tok0 + i) * p.h_kv * kD + (int64_t)h * kD + c];
+      const int64_t at = (((slot / kPage) * p.h_kv + h) * kD + c) * kPage + slot % kPage;
+      p.v_codes[at] = (uint8_t)e4m3_rne_sat(bf16_to_f32(vb));
+      if (p.pv == 1) reinterpret_cast<uint16_t*>(p.v_aux)[at] = vb;
     }
   }
   if (!p.smooth) return;

@@ -47,9 +47,13 @@ class Run:
     """One quantize (+ optional prefill) through the HIP path and the oracle."""
 
     def __init__(self, orc, mp, seed, seqlens, h_q, h_kv, outliers=True, smooth=True,
-                 tscale_unit=False, shuffle=True, device="cuda", mxfp4=False):
+                 tscale_unit=False, shuffle=True, device="cuda", mxfp4=False, pv=None):
+        """pv: None, "bf16" or "nvfp4" (precision assignment of the PV product)."""
         self.orc, self.mp = orc, mp
         self.mxfp4 = mxfp4
+        self.pv = pv
+        self.pv_flag = {None: 0, "bf16": mp.PV_BF16, "nvfp4": mp.PV_NVFP4}[pv]
+        self.pv_orc = {None: 0, "bf16": orc.PV_BF16, "nvfp4": orc.PV_NVFP4}[pv]
         self.seqlens = list(seqlens)
         self.h_q, self.h_kv = h_q, h_kv
         self.smooth = smooth
@@ -64,11 +68,11 @@ class Run:
             if cu[-1] > 0 else np.zeros(0, np.int64)
         self.slots = slots
         flags = (mp.SMOOTH if smooth else 0) | mp.COMPUTE_STATS | (mp.TSCALE_UNIT if tscale_unit else 0) \
-            | (mp.MXFP4 if mxfp4 else 0)
+            | (mp.MXFP4 if mxfp4 else 0) | self.pv_flag
         self.flags = flags
         # HIP path
         T = int(cu[-1])
-        self.cache = mp.PagedCache(max(self.n_pages, 1), h_q, h_kv, device, smooth=True)
+        self.cache = mp.PagedCache(max(self.n_pages, 1), h_q, h_kv, device, smooth=True, pv=self.pv_flag)
         self.stats = mp.SeqStats(B, h_q, h_kv, device)
         self.qq = mp.QuantQ(T, B, h_q, device)
         dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
@@ -81,7 +85,7 @@ class Run:
         self.ref = orc.quantize_qk(bits(q), bits(k), bits(v), cu, slots, max(self.n_pages, 1),
                                    (orc.SMOOTH if smooth else 0) | orc.COMPUTE_STATS |
                                    (orc.TSCALE_UNIT if tscale_unit else 0) |
-                                   (orc.MXFP4 if mxfp4 else 0))
+                                   (orc.MXFP4 if mxfp4 else 0) | self.pv_orc)
 
     def gpu_quant(self):
         c = self.cache
@@ -107,7 +111,8 @@ class Run:
         out = torch.full((T, self.h_q, 128), float("nan"), dtype=torch.bfloat16, device="cuda")
         mp.prefill(self.qq, self.cache, self.stats, self.cu_d, dev(q_start), dev(kv_len),
                    dev(self.pt), out, max(self.seqlens),
-                   (mp.SMOOTH if self.smooth else 0) | (mp.MXFP4 if self.mxfp4 else 0) | extra_flags)
+                   (mp.SMOOTH if self.smooth else 0) | (mp.MXFP4 if self.mxfp4 else 0) | self.pv_flag
+                   | extra_flags)
         torch.cuda.synchronize()
         return bits(out)
 
@@ -118,5 +123,5 @@ class Run:
         r = self.ref
         o16, o64 = self.orc.prefill(r["cache"], self.pt, kv_len, r["k_tscale"], r["q_codes"],
                                     r["q_scales"], r["q_tscale"], self.cu, q_start, items,
-                                    smooth=self.smooth, mxfp4=self.mxfp4)
+                                    smooth=self.smooth, mxfp4=self.mxfp4, pv=self.pv_orc)
         return o16, o64

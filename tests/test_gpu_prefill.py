@@ -176,3 +176,30 @@ def test_prefill_mxfp4_llama_sampled(orc, mp):
     rows = np.unique(np.concatenate([np.arange(0, 200), rng.integers(0, n, 150), [n - 1]]))
     items = np.array([(0, int(i), h) for i in rows for h in range(0, 32, 5)], np.int32)
     _check(run, out, items, label="mxfp4 llama sampled")
+
+
+@pytest.mark.parametrize("pv,smooth", [("bf16", True), ("bf16", False), ("nvfp4", True), ("nvfp4", False)])
+def test_prefill_pv_precisions(orc, mp, pv, smooth):
+    """The PV precision assignments compared in Sec. 3.1 (BF16 P and V; NVFP4 P
+    with dynamic per-16-key scales and NVFP4 V) over a ragged GQA batch, every
+    output row against the oracle; repeated launches give identical bytes."""
+    print(f"case: pv={pv} smooth={smooth}", flush=True)
+    seqlens = [1, 130, 300, 513]
+    run = H.Run(orc, mp, 53, seqlens, 8, 2, outliers=True, smooth=smooth, pv=pv)
+    out = run.prefill_gpu()
+    _check(run, out, _all_items(seqlens, 8), label=f"pv={pv} smooth={smooth}")
+    for _ in range(3):
+        assert np.array_equal(run.prefill_gpu(), out)
+
+
+@pytest.mark.parametrize("pv", ["bf16", "nvfp4"])
+def test_prefill_pv_llama_sampled(orc, mp, pv):
+    """PV precision assignments on the Llama-shaped 16384-token workload, sampled rows."""
+    print(f"case: pv={pv} llama 16384 sampled", flush=True)
+    n = 16384
+    run = H.Run(orc, mp, 2, [n], 32, 8, outliers=True, pv=pv)
+    out = run.prefill_gpu()
+    rng = np.random.default_rng(3)
+    rows = np.unique(np.concatenate([np.arange(0, 130), rng.integers(0, n, 120), [n - 1]]))
+    items = np.array([(0, int(i), h) for i in rows for h in range(0, 32, 7)], np.int32)
+    _check(run, out, items, label=f"pv={pv} llama sampled")

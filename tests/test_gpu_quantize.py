@@ -184,3 +184,19 @@ def test_quantize_empty_and_short_sequences(orc, mp):
     print("case: ragged batch [0, 5, 129, 0, 256]", flush=True)
     run = H.Run(orc, mp, 19, [0, 5, 129, 0, 256], 4, 2, outliers=True)
     _assert_quant_equal(run)
+
+
+@pytest.mark.parametrize("pv", ["bf16", "nvfp4"])
+def test_quantize_pv_copies(orc, mp, pv):
+    """The V copies of the PV precision characterization (BF16 rows, or NVFP4
+    16-key groups per channel in two planes) bit for bit, next to the unchanged
+    FP8 cache, over a ragged batch with shuffled pages and partial last pages."""
+    print(f"case: quantize pv={pv}", flush=True)
+    run = H.Run(orc, mp, 47, [1, 200, 333, 64, 130], 8, 2, outliers=True, pv=pv)
+    _assert_quant_equal(run)
+    got = run.cache.v_aux
+    got = (H.bits(got) if got.dtype == torch.bfloat16 else got.cpu().numpy()).reshape(-1)
+    ref = np.asarray(run.ref["cache"]["v_aux"]).reshape(-1)
+    assert got.shape == ref.shape
+    bad = np.nonzero(got != ref)[0]
+    assert bad.size == 0, (bad[:5], got[bad[:5]], ref[bad[:5]])
