@@ -84,6 +84,8 @@ def parse():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-direct", action="store_true", help="skip the unsmoothed prefill variant")
     ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant runs")
+    ap.add_argument("--no-precision", action="store_true",
+                    help="skip the BF16 / NVFP4 PV precision-assignment runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-accuracy", action="store_true",
                     help="skip the error report against FP64 unquantized attention")
@@ -113,7 +115,7 @@ class Timer:
         return self.s.elapsed_time(self.e)
 
 
-def setup_prefill(torch, np, mp, W, seq, smooth, mx=False):
+def setup_prefill(torch, np, mp, W, seq, smooth, mx=False, pv=0):
     wl = W.qwen_prefill(seq)
     dev = "cuda"
     q, k, v = W.gen_qkv(wl.seed, [seq], wl.h_q, wl.h_kv, wl.outliers, dev)
@@ -123,10 +125,10 @@ def setup_prefill(torch, np, mp, W, seq, smooth, mx=False):
     st = dict(wl=wl, q=q, k=k, v=v, pt=pt, pt_d=d(pt), n_pages=n_pages,
               cu=d(np.array([0, seq], np.int32)), slots=d(slots),
               q_start=d(np.zeros(1, np.int32)), kv_len=d(np.array([seq], np.int32)),
-              cache=mp.PagedCache(n_pages, wl.h_q, wl.h_kv, dev, smooth=smooth),
+              cache=mp.PagedCache(n_pages, wl.h_q, wl.h_kv, dev, smooth=smooth, pv=pv),
               stats=mp.SeqStats(1, wl.h_q, wl.h_kv, dev), qq=mp.QuantQ(seq, 1, wl.h_q, dev),
               out=torch.empty((seq, wl.h_q, 128), dtype=torch.bfloat16, device=dev),
-              flags=(mp.SMOOTH if smooth else 0) | (mp.MXFP4 if mx else 0))
+              flags=(mp.SMOOTH if smooth else 0) | (mp.MXFP4 if mx else 0) | pv)
     return st
 
 
@@ -421,6 +423,30 @@ def main():
                                     "quant_ms": mq_ms, "layer_ms": mq_ms + mx_ms}
             del sm
             torch.cuda.empty_cache()
+
+    if not args.no_prefill and not args.no_precision:
+        # the other precision assignments of the PV product (Sec. 3.1, Fig. 3a)
+        pa = {"nvfp4_fp8": {"ms": prefill_ms, "tflops": flops / (prefill_ms * 1e-3) / 1e12}}
+        for name, pv in (("nvfp4_bf16", mp.PV_BF16), ("nvfp4_nvfp4", mp.PV_NVFP4)):
+            log(f"prefill, PV precision {name} ...")
+            sp = setup_prefill(torch, np, mp, W, seq, smooth=True, pv=pv)
+            for _ in range(max(args.warmup, 1)):
+                run_quant(mp, sp)
+                run_prefill(mp, sp)
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(args.steps):
+                with Timer(torch) as t2:
+                    run_prefill(mp, sp)
+                ts.append(t2)
+            torch.cuda.synchronize()
+            ms = sum(t.ms() for t in ts) / args.steps
+            pa[name] = {"ms": ms, "tflops": flops / (ms * 1e-3) / 1e12, "time_vs_fp8": ms / prefill_ms}
+            if acc:
+                acc[name] = error_vs_fp64(np, sp["out"], ref64)
+            del sp
+            torch.cuda.empty_cache()
+        res["precision_assignments"] = pa
 
     if acc:
         res["accuracy_vs_fp64"] = acc
