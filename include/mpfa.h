@@ -261,6 +261,33 @@ mpfa_status mpfa_decode_paged(const mpfa_decode_args* args, void* workspace, siz
                               mpfa_stream_t stream);
 
 /* ------------------------------------------------------------------------ */
+/* Mixed serving step in one launch (Sec. 7.3; prefill and decode requests    */
+/* of one step served together)                                               */
+/* ------------------------------------------------------------------------ */
+/*
+ * Runs the causal prefill described by `prefill` and the split-KV decode
+ * described by `decode` in a single kernel launch, merge included: prefill
+ * query tiles (matrix-bound) and decode partitions (HBM-bound) are
+ * interleaved over the grid so both resources work in the same interval.
+ * Results are bit-identical to mpfa_prefill followed by mpfa_decode_paged
+ * with the same arguments.  Both parts must use the same MPFA_SMOOTH /
+ * MPFA_MXFP4 setting (else MPFA_ERR_INVALID); the prefill flags may not
+ * contain MPFA_SEED_INIT, MPFA_SEED_ELEMWISE or the PV characterization
+ * flags (MPFA_ERR_UNSUPPORTED).  Each part is validated as by its own entry
+ * point.
+ * workspace: caller-owned device memory of at least
+ * mpfa_mixed_workspace_size(decode batch, h_q, h_kv, max_partitions) bytes:
+ * the decode partition states, then one 32-bit counter per (sequence, KV
+ * head).  The counters must be zero before the first call on a workspace
+ * (allocate it zeroed); every completed call leaves them zero again.  Calls
+ * that share a workspace must not overlap.
+ */
+mpfa_status mpfa_mixed_workspace_size(int32_t batch, int32_t h_q, int32_t h_kv,
+                                      int32_t max_partitions, size_t* bytes);
+mpfa_status mpfa_mixed_step(const mpfa_prefill_args* prefill, const mpfa_decode_args* decode,
+                            void* workspace, size_t workspace_bytes, mpfa_stream_t stream);
+
+/* ------------------------------------------------------------------------ */
 /* Utilities                                                                  */
 /* ------------------------------------------------------------------------ */
 /* Element-wise device conversions, exposed so that their rounding can be

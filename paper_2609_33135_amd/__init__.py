@@ -18,8 +18,8 @@ PV_BF16, PV_NVFP4 = 64, 128
 HEAD_DIM, PAGE, TILE = 128, 64, 128
 
 EXPORTED = ("mpfa_quantize_qk", "mpfa_prefill", "mpfa_decode_workspace_size",
-            "mpfa_decode_choose_partition", "mpfa_decode_paged", "mpfa_convert",
-            "mpfa_status_string", "mpfa_version")
+            "mpfa_decode_choose_partition", "mpfa_decode_paged", "mpfa_mixed_workspace_size",
+            "mpfa_mixed_step", "mpfa_convert", "mpfa_status_string", "mpfa_version")
 
 
 class MpfaError(RuntimeError):
@@ -83,6 +83,12 @@ def lib():
                                                    C.POINTER(C.c_int32)]
         L.mpfa_decode_paged.restype = C.c_int
         L.mpfa_decode_paged.argtypes = [C.POINTER(DecodeArgs), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.mpfa_mixed_workspace_size.restype = C.c_int
+        L.mpfa_mixed_workspace_size.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                                C.POINTER(C.c_size_t)]
+        L.mpfa_mixed_step.restype = C.c_int
+        L.mpfa_mixed_step.argtypes = [C.POINTER(PrefillArgs), C.POINTER(DecodeArgs), C.c_void_p,
+                                      C.c_size_t, C.c_void_p]
         L.mpfa_convert.restype = C.c_int
         L.mpfa_convert.argtypes = [C.c_int32, C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p]
         L.mpfa_status_string.restype = C.c_char_p
@@ -214,6 +220,41 @@ def decode_paged(qq: QuantQ, cache: PagedCache, stats: SeqStats, kv_len, page_ta
     _check(lib().mpfa_decode_paged(C.byref(a), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream)),
            "mpfa_decode_paged")
+
+
+def mixed_workspace_size(batch: int, h_q: int, h_kv: int, max_partitions: int) -> int:
+    n = C.c_size_t(0)
+    _check(lib().mpfa_mixed_workspace_size(batch, h_q, h_kv, max_partitions, C.byref(n)),
+           "mpfa_mixed_workspace_size")
+    return n.value
+
+
+def mixed_step(pre: dict, dec: dict, workspace, flags: int, stream=None):
+    """mpfa_mixed_step: one launch for a prefill (keyword arguments of prefill())
+    and a decode (keyword arguments of decode_paged() without the workspace and
+    flags); the workspace must start zeroed (torch.zeros) and stays zeroed."""
+    qq, cache, stats = pre["qq"], pre["cache"], pre["stats"]
+    pa = PrefillArgs(batch=pre["cu_seqlens_q"].numel() - 1, h_q=qq.codes.shape[1], h_kv=cache.h_kv,
+                     head_dim=HEAD_DIM, max_seqlen_q=pre["max_seqlen_q"],
+                     max_pages=pre["page_table"].shape[1], flags=flags,
+                     cu_seqlens_q=_ptr(pre["cu_seqlens_q"]), q_start=_ptr(pre["q_start"]),
+                     kv_len=_ptr(pre["kv_len"]), page_table=_ptr(pre["page_table"]),
+                     q_codes=_ptr(qq.codes), q_scales=_ptr(qq.scales), q_tscale=_ptr(qq.tscale),
+                     k_codes=_ptr(cache.k_codes), k_scales=_ptr(cache.k_scales),
+                     v_codes=_ptr(cache.v_codes), ds=_ptr(cache.ds), k_tscale=_ptr(stats.k_tscale),
+                     out=_ptr(pre["out"]), v_aux=None, num_pages=cache.num_pages)
+    qd, dcache, dstats = dec["qq"], dec["cache"], dec["stats"]
+    da = DecodeArgs(batch=dec["kv_len"].numel(), h_q=qd.codes.shape[1], h_kv=dcache.h_kv,
+                    head_dim=HEAD_DIM, max_pages=dec["page_table"].shape[1],
+                    partition_tokens=dec["partition_tokens"], max_partitions=dec["max_partitions"],
+                    flags=flags, kv_len=_ptr(dec["kv_len"]), page_table=_ptr(dec["page_table"]),
+                    q_codes=_ptr(qd.codes), q_scales=_ptr(qd.scales), q_tscale=_ptr(qd.tscale),
+                    k_codes=_ptr(dcache.k_codes), k_scales=_ptr(dcache.k_scales),
+                    v_codes=_ptr(dcache.v_codes), ds=_ptr(dcache.ds), k_tscale=_ptr(dstats.k_tscale),
+                    out=_ptr(dec["out"]))
+    _check(lib().mpfa_mixed_step(C.byref(pa), C.byref(da), _ptr(workspace),
+                                 workspace.numel() * workspace.element_size(), _stream(stream)),
+           "mpfa_mixed_step")
 
 
 def convert(fmt: int, x, out, stream=None):

@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmpfa.so")
 
-SOURCES = ["api.cpp", "quantize.hip", "prefill.hip", "decode.hip"]
+SOURCES = ["api.cpp", "quantize.hip", "prefill.hip", "decode.hip", "mixed.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CLANG = os.environ.get("MPFA_CLANG", "/opt/rocm/lib/llvm/bin/clang++")
 ARCH = os.environ.get("MPFA_ARCH", "gfx950")

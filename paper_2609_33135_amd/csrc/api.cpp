@@ -21,7 +21,112 @@ bool heads_ok(int h_q, int h_kv) {
   return h_q >= 1 && h_kv >= 1 && h_q <= MPFA_MAX_HEADS && h_kv <= kMaxKvHeads && h_q % h_kv == 0;
 }
 
+// partition counters of the fused step follow the decode states, 256-byte aligned
+size_t mixed_counter_offset(size_t state_bytes) { return (state_bytes + 255) / 256 * 256; }
+
 }  // namespace
+
+// Host-side validation of the prefill arguments and their launch parameters.
+static mpfa_status prefill_params(const mpfa_prefill_args* a, mpfa::PrefillParams& p) {
+  if (!a) return MPFA_ERR_INVALID;
+  if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
+  if (a->batch < 1 || a->max_seqlen_q < 0 || a->max_pages < 1) return MPFA_ERR_INVALID;
+  if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
+  if (a->flags & ~(MPFA_SMOOTH | MPFA_SEED_INIT | MPFA_SEED_ELEMWISE | MPFA_MXFP4 | MPFA_PV_BF16 |
+                   MPFA_PV_NVFP4))
+    return MPFA_ERR_INVALID;
+  if ((a->flags & MPFA_SEED_INIT) && (a->flags & MPFA_SEED_ELEMWISE)) return MPFA_ERR_INVALID;
+  const uint32_t pvp = a->flags & (MPFA_PV_BF16 | MPFA_PV_NVFP4);
+  if (pvp == (MPFA_PV_BF16 | MPFA_PV_NVFP4) || (pvp && !a->v_aux)) return MPFA_ERR_INVALID;
+  if ((pvp & MPFA_PV_NVFP4) && a->num_pages < 1) return MPFA_ERR_INVALID;
+  if (pvp && (a->flags & (MPFA_MXFP4 | MPFA_SEED_INIT | MPFA_SEED_ELEMWISE))) return MPFA_ERR_UNSUPPORTED;
+  const bool smooth = a->flags & MPFA_SMOOTH;
+  if (!a->cu_seqlens_q || !a->q_start || !a->kv_len || !a->page_table || !a->q_codes ||
+      !a->q_scales || !a->q_tscale || !a->k_codes || !a->k_scales || !a->v_codes ||
+      !a->k_tscale || !a->out || (smooth && !a->ds))
+    return MPFA_ERR_INVALID;
+  const int64_t n_qtiles = ((int64_t)a->max_seqlen_q + kPrefillRows - 1) / kPrefillRows;
+  if (n_qtiles * a->h_q * (int64_t)a->batch > INT32_MAX) return MPFA_ERR_INVALID;
+
+  p = mpfa::PrefillParams{};
+  p.batch = a->batch;
+  p.h_q = a->h_q;
+  p.h_kv = a->h_kv;
+  p.max_pages = a->max_pages;
+  p.n_qtiles = (int)n_qtiles;
+  p.smooth = smooth;
+  p.seed_init = (a->flags & MPFA_SEED_INIT) != 0;
+  p.seed_elem = (a->flags & MPFA_SEED_ELEMWISE) != 0;
+  p.pv = (a->flags & MPFA_PV_BF16) ? 1 : (a->flags & MPFA_PV_NVFP4) ? 2 : 0;
+  p.v_aux = static_cast<const uint8_t*>(a->v_aux);
+  p.num_pages = a->num_pages;
+  p.mx = (a->flags & MPFA_MXFP4) != 0;
+  p.xcd_remap = (a->h_kv % 8) == 0;
+  p.lam = kLambda;
+  p.cu_seqlens_q = a->cu_seqlens_q;
+  p.q_start = a->q_start;
+  p.kv_len = a->kv_len;
+  p.page_table = a->page_table;
+  p.q_codes = a->q_codes;
+  p.q_scales = a->q_scales;
+  p.q_tscale = a->q_tscale;
+  p.k_codes = a->k_codes;
+  p.k_scales = a->k_scales;
+  p.v_codes = a->v_codes;
+  p.ds = static_cast<const uint16_t*>(a->ds);
+  p.k_tscale = a->k_tscale;
+  p.out = static_cast<uint16_t*>(a->out);
+  return MPFA_OK;
+}
+
+
+// Host-side validation of the decode arguments and their launch parameters.
+static mpfa_status decode_params(const mpfa_decode_args* a, void* workspace, size_t workspace_bytes,
+                                 mpfa::DecodeParams& p) {
+  if (!a) return MPFA_ERR_INVALID;
+  if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
+  if (a->batch < 1 || a->batch > 65535 || a->max_pages < 1 || a->max_partitions < 1)
+    return MPFA_ERR_INVALID;
+  if (a->partition_tokens < MPFA_KV_TILE || a->partition_tokens % MPFA_KV_TILE)
+    return MPFA_ERR_INVALID;
+  if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
+  if (a->h_q / a->h_kv > kMaxDecodeGroup) return MPFA_ERR_UNSUPPORTED;
+  if (a->flags & (MPFA_PV_BF16 | MPFA_PV_NVFP4)) return MPFA_ERR_UNSUPPORTED;
+  if (a->flags & ~(MPFA_SMOOTH | MPFA_MXFP4)) return MPFA_ERR_INVALID;
+  const bool smooth = a->flags & MPFA_SMOOTH;
+  if (!a->kv_len || !a->page_table || !a->q_codes || !a->q_scales || !a->q_tscale ||
+      !a->k_codes || !a->k_scales || !a->v_codes || !a->k_tscale || !a->out || (smooth && !a->ds))
+    return MPFA_ERR_INVALID;
+  size_t need = 0;
+  if (mpfa_decode_workspace_size(a->batch, a->h_q, a->max_partitions, &need) != MPFA_OK)
+    return MPFA_ERR_INVALID;
+  if (!workspace || workspace_bytes < need) return MPFA_ERR_WORKSPACE;
+
+  p = mpfa::DecodeParams{};
+  p.batch = a->batch;
+  p.h_q = a->h_q;
+  p.h_kv = a->h_kv;
+  p.max_pages = a->max_pages;
+  p.partition_tokens = a->partition_tokens;
+  p.max_partitions = a->max_partitions;
+  p.smooth = smooth;
+  p.mx = (a->flags & MPFA_MXFP4) != 0;
+  p.lam = kLambda;
+  p.kv_len = a->kv_len;
+  p.page_table = a->page_table;
+  p.q_codes = a->q_codes;
+  p.q_scales = a->q_scales;
+  p.q_tscale = a->q_tscale;
+  p.k_codes = a->k_codes;
+  p.k_scales = a->k_scales;
+  p.v_codes = a->v_codes;
+  p.ds = static_cast<const uint16_t*>(a->ds);
+  p.k_tscale = a->k_tscale;
+  p.ws = static_cast<float*>(workspace);
+  p.out = static_cast<uint16_t*>(a->out);
+  return MPFA_OK;
+}
+
 
 extern "C" {
 
@@ -93,54 +198,9 @@ mpfa_status mpfa_quantize_qk(const mpfa_quant_args* a, mpfa_stream_t stream) {
 }
 
 mpfa_status mpfa_prefill(const mpfa_prefill_args* a, mpfa_stream_t stream) {
-  if (!a) return MPFA_ERR_INVALID;
-  if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
-  if (a->batch < 1 || a->max_seqlen_q < 0 || a->max_pages < 1) return MPFA_ERR_INVALID;
-  if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
-  if (a->flags & ~(MPFA_SMOOTH | MPFA_SEED_INIT | MPFA_SEED_ELEMWISE | MPFA_MXFP4 | MPFA_PV_BF16 |
-                   MPFA_PV_NVFP4))
-    return MPFA_ERR_INVALID;
-  if ((a->flags & MPFA_SEED_INIT) && (a->flags & MPFA_SEED_ELEMWISE)) return MPFA_ERR_INVALID;
-  const uint32_t pvp = a->flags & (MPFA_PV_BF16 | MPFA_PV_NVFP4);
-  if (pvp == (MPFA_PV_BF16 | MPFA_PV_NVFP4) || (pvp && !a->v_aux)) return MPFA_ERR_INVALID;
-  if ((pvp & MPFA_PV_NVFP4) && a->num_pages < 1) return MPFA_ERR_INVALID;
-  if (pvp && (a->flags & (MPFA_MXFP4 | MPFA_SEED_INIT | MPFA_SEED_ELEMWISE))) return MPFA_ERR_UNSUPPORTED;
-  const bool smooth = a->flags & MPFA_SMOOTH;
-  if (!a->cu_seqlens_q || !a->q_start || !a->kv_len || !a->page_table || !a->q_codes ||
-      !a->q_scales || !a->q_tscale || !a->k_codes || !a->k_scales || !a->v_codes ||
-      !a->k_tscale || !a->out || (smooth && !a->ds))
-    return MPFA_ERR_INVALID;
-  const int64_t n_qtiles = ((int64_t)a->max_seqlen_q + kPrefillRows - 1) / kPrefillRows;
-  if (n_qtiles * a->h_q * (int64_t)a->batch > INT32_MAX) return MPFA_ERR_INVALID;
-
-  mpfa::PrefillParams p{};
-  p.batch = a->batch;
-  p.h_q = a->h_q;
-  p.h_kv = a->h_kv;
-  p.max_pages = a->max_pages;
-  p.n_qtiles = (int)n_qtiles;
-  p.smooth = smooth;
-  p.seed_init = (a->flags & MPFA_SEED_INIT) != 0;
-  p.seed_elem = (a->flags & MPFA_SEED_ELEMWISE) != 0;
-  p.pv = (a->flags & MPFA_PV_BF16) ? 1 : (a->flags & MPFA_PV_NVFP4) ? 2 : 0;
-  p.v_aux = static_cast<const uint8_t*>(a->v_aux);
-  p.num_pages = a->num_pages;
-  p.mx = (a->flags & MPFA_MXFP4) != 0;
-  p.xcd_remap = (a->h_kv % 8) == 0;
-  p.lam = kLambda;
-  p.cu_seqlens_q = a->cu_seqlens_q;
-  p.q_start = a->q_start;
-  p.kv_len = a->kv_len;
-  p.page_table = a->page_table;
-  p.q_codes = a->q_codes;
-  p.q_scales = a->q_scales;
-  p.q_tscale = a->q_tscale;
-  p.k_codes = a->k_codes;
-  p.k_scales = a->k_scales;
-  p.v_codes = a->v_codes;
-  p.ds = static_cast<const uint16_t*>(a->ds);
-  p.k_tscale = a->k_tscale;
-  p.out = static_cast<uint16_t*>(a->out);
+  mpfa::PrefillParams p;
+  const mpfa_status st = prefill_params(a, p);
+  if (st != MPFA_OK) return st;
   return mpfa::launch_prefill(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
                                                                                        : MPFA_ERR_HIP;
 }
@@ -172,50 +232,54 @@ mpfa_status mpfa_decode_choose_partition(int32_t batch, const int32_t* kv_len_ho
 
 mpfa_status mpfa_decode_paged(const mpfa_decode_args* a, void* workspace, size_t workspace_bytes,
                               mpfa_stream_t stream) {
-  if (!a) return MPFA_ERR_INVALID;
-  if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
-  if (a->batch < 1 || a->batch > 65535 || a->max_pages < 1 || a->max_partitions < 1)
-    return MPFA_ERR_INVALID;
-  if (a->partition_tokens < MPFA_KV_TILE || a->partition_tokens % MPFA_KV_TILE)
-    return MPFA_ERR_INVALID;
-  if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
-  if (a->h_q / a->h_kv > kMaxDecodeGroup) return MPFA_ERR_UNSUPPORTED;
-  if (a->flags & (MPFA_PV_BF16 | MPFA_PV_NVFP4)) return MPFA_ERR_UNSUPPORTED;
-  if (a->flags & ~(MPFA_SMOOTH | MPFA_MXFP4)) return MPFA_ERR_INVALID;
-  const bool smooth = a->flags & MPFA_SMOOTH;
-  if (!a->kv_len || !a->page_table || !a->q_codes || !a->q_scales || !a->q_tscale ||
-      !a->k_codes || !a->k_scales || !a->v_codes || !a->k_tscale || !a->out || (smooth && !a->ds))
-    return MPFA_ERR_INVALID;
-  size_t need = 0;
-  if (mpfa_decode_workspace_size(a->batch, a->h_q, a->max_partitions, &need) != MPFA_OK)
-    return MPFA_ERR_INVALID;
-  if (!workspace || workspace_bytes < need) return MPFA_ERR_WORKSPACE;
-
-  mpfa::DecodeParams p{};
-  p.batch = a->batch;
-  p.h_q = a->h_q;
-  p.h_kv = a->h_kv;
-  p.max_pages = a->max_pages;
-  p.partition_tokens = a->partition_tokens;
-  p.max_partitions = a->max_partitions;
-  p.smooth = smooth;
-  p.mx = (a->flags & MPFA_MXFP4) != 0;
-  p.lam = kLambda;
-  p.kv_len = a->kv_len;
-  p.page_table = a->page_table;
-  p.q_codes = a->q_codes;
-  p.q_scales = a->q_scales;
-  p.q_tscale = a->q_tscale;
-  p.k_codes = a->k_codes;
-  p.k_scales = a->k_scales;
-  p.v_codes = a->v_codes;
-  p.ds = static_cast<const uint16_t*>(a->ds);
-  p.k_tscale = a->k_tscale;
-  p.ws = static_cast<float*>(workspace);
-  p.out = static_cast<uint16_t*>(a->out);
+  mpfa::DecodeParams p;
+  const mpfa_status st = decode_params(a, workspace, workspace_bytes, p);
+  if (st != MPFA_OK) return st;
   return mpfa::launch_decode(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
                                                                                       : MPFA_ERR_HIP;
 }
+
+mpfa_status mpfa_mixed_workspace_size(int32_t batch, int32_t h_q, int32_t h_kv, int32_t max_partitions,
+                                      size_t* bytes) {
+  size_t states = 0;
+  if (!bytes || h_kv < 1 || mpfa_decode_workspace_size(batch, h_q, max_partitions, &states) != MPFA_OK)
+    return MPFA_ERR_INVALID;
+  *bytes = mixed_counter_offset(states) + (size_t)batch * (size_t)h_kv * sizeof(uint32_t);
+  return MPFA_OK;
+}
+
+mpfa_status mpfa_mixed_step(const mpfa_prefill_args* prefill, const mpfa_decode_args* decode,
+                            void* workspace, size_t workspace_bytes, mpfa_stream_t stream) {
+  if (!prefill || !decode) return MPFA_ERR_INVALID;
+  // the fused kernel runs the method's placements only (rank-one seed or none,
+  // FP8 PV), with one smoothing / format setting for both parts
+  if (prefill->flags & (MPFA_SEED_INIT | MPFA_SEED_ELEMWISE | MPFA_PV_BF16 | MPFA_PV_NVFP4))
+    return MPFA_ERR_UNSUPPORTED;
+  if ((prefill->flags & (MPFA_SMOOTH | MPFA_MXFP4)) != (decode->flags & (MPFA_SMOOTH | MPFA_MXFP4)))
+    return MPFA_ERR_INVALID;
+  mpfa::MixedParams m{};
+  mpfa_status st = prefill_params(prefill, m.pre);
+  if (st != MPFA_OK) return st;
+  size_t need = 0;
+  if (mpfa_mixed_workspace_size(decode->batch, decode->h_q, decode->h_kv, decode->max_partitions, &need) !=
+      MPFA_OK)
+    return MPFA_ERR_INVALID;
+  if (!workspace || workspace_bytes < need) return MPFA_ERR_WORKSPACE;
+  st = decode_params(decode, workspace, workspace_bytes, m.dec);
+  if (st != MPFA_OK) return st;
+  size_t states = 0;
+  mpfa_decode_workspace_size(decode->batch, decode->h_q, decode->max_partitions, &states);
+  m.counters = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(workspace) + mixed_counter_offset(states));
+  const int64_t n_pre = (int64_t)m.pre.n_qtiles * m.pre.h_q * m.pre.batch;
+  const int64_t n_dec = ((int64_t)m.dec.batch * m.dec.h_kv * m.dec.max_partitions + 7) / 8;
+  if (n_pre + n_dec > INT32_MAX) return MPFA_ERR_INVALID;
+  m.n_pre_blocks = (int)n_pre;
+  m.n_dec_blocks = (int)n_dec;
+  m.stride = n_dec > 0 ? (int)((n_pre + n_dec) / n_dec) : (int)(n_pre + n_dec + 1);
+  return mpfa::launch_mixed(m, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
+                                                                                    : MPFA_ERR_HIP;
+}
+
 
 mpfa_status mpfa_convert(int32_t fmt, const float* x, int64_t n, uint8_t* out, mpfa_stream_t stream) {
   if (fmt < 0 || fmt > 3 || n < 0 || (n > 0 && (!x || !out))) return MPFA_ERR_INVALID;

@@ -81,7 +81,18 @@ struct DecodeParams {
   uint16_t* out;
 };
 
+// One launch for a step of prefill items and decode partitions (with the merge).
+struct MixedParams {
+  PrefillParams pre;
+  DecodeParams dec;
+  int n_pre_blocks;   // prefill work items (query tiles x heads x sequences)
+  int n_dec_blocks;   // groups of 8 decode work items
+  int stride;         // a decode group every `stride` blocks
+  uint32_t* counters; // [dec.batch][dec.h_kv] partition counters, zero between calls
+};
+
 hipError_t launch_quantize(const QuantParams& p, hipStream_t stream);
+hipError_t launch_mixed(const MixedParams& m, hipStream_t stream);
 hipError_t launch_convert(int fmt, const float* x, int64_t n, uint8_t* out, hipStream_t stream);
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream);

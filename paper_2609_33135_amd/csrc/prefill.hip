@@ -18,504 +18,16 @@
 // The key order inside a 16-row MFMA block is permuted so that the 32 keys a
 // lane holds after the QK product are contiguous: MFMA row r of key block mb
 // is key 32*(r/4) + 4*mb + r%4.
-#include "mpfa_device.h"
-#include "mpfa_internal.h"
+#include "prefill_body.h"
 
 namespace mpfa {
 
 namespace {
 
-constexpr int kWaves = 8;
-constexpr int kNB = 2;                       // 16-row query blocks per wave
-constexpr int kQRows = kWaves * kNB * 16;    // 256 query rows per workgroup
-constexpr int kThreads = kWaves * 64;
-
-// Precision of the PV product: the method's FP8 (P * 448 and V in E4M3), or
-// the two other assignments compared in Sec. 3.1 / Fig. 3a, BF16 P and V, and
-// NVFP4 P (2688 P quantized per 16 keys with dynamic E4M3 scales) with NVFP4 V
-// (16-key groups per channel, tensor scale 1), both on FP16 / BF16 MFMA after
-// exact dequantization.
-enum PvMode { kPvFp8 = 0, kPvBf16 = 1, kPvNvfp4 = 2 };
-
-template <int PV>
-struct PrefillSmemT {
-  // NVFP4: FP16 [key][128], 16-byte chunks XOR-swizzled per key.  MXFP4: raw
-  // codes [key][64] (chunks swizzled by mx_swz) in the first 8 KB, then the
-  // E8M0 scales transposed to [MFMA row][32-channel block][16-key block].
-  uint8_t k[kTile * 256];
-  // FP8: [channel][key] bytes, 16-byte chunks XOR-swizzled per channel (v_swz).
-  // BF16 / NVFP4: [channel][key] BF16 or exact FP16, 256-byte rows of 16
-  // chunks, chunk c of channel d stored at position c ^ (d & 15).
-  uint8_t v[kD * kTile * (PV == kPvFp8 ? 1 : 2)];
-  uint16_t ds[kTile];       // BF16 seed values in accumulator units
-};
-
-// chunk swizzles: conflict-free 16-byte reads for the MFMA operand patterns
-__device__ __forceinline__ int k_swz(int key) { return (((key >> 5) << 2) | (key & 3)) & 15; }
-__device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 7; }
-__device__ __forceinline__ int mx_swz(int key) { return ((key >> 1) & 1) | (((key >> 5) & 1) << 1); }
-constexpr int kMxScaleOff = kTile * 64;   // byte offset of the MXFP4 scales in PrefillSmem::k
-
-__device__ __forceinline__ u32x4 zero_tail(u32x4 w, int nvalid) {
-  // keep bytes [0, nvalid) of the 16-byte word
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int keep = nvalid - 4 * i;
-    uint32_t mask = keep >= 4 ? 0xFFFFFFFFu : (keep <= 0 ? 0u : ((1u << (8 * keep)) - 1u));
-    w[i] &= mask;
-  }
-  return w;
-}
-
-// Raw bytes of one KV tile held in registers between the global load and the
-// LDS store (software pipelining: the next tile is fetched while the current
-// one is computed).
-template <int PV>
-struct TileRegs {
-  u32x4 kc;        // 16 NVFP4 code bytes: key t/4, channels 32*(t%4) .. +31
-  uint32_t ksc;    // their two E4M3 group scales
-  // channel t/4, keys 32*(t%4) .. +31 of the tile: 32 FP8 bytes, 32 BF16
-  // values, or 32 E2M1 codes (16 bytes)
-  static constexpr int kVWords = PV == kPvFp8 ? 2 : (PV == kPvBf16 ? 4 : 1);
-  u32x4 v[kVWords];
-  uint32_t vsc;    // NVFP4 V: the two E4M3 scales of those keys
-  uint32_t ds;     // BF16 Delta_S of key t (threads 0..127)
-};
-
-template <bool MX, int PV>
-__device__ __forceinline__ void fetch_tile(TileRegs<PV>& r, const PrefillParams& p, const int32_t* pt,
-                                           int hk, int h, int j, int kvl) {
-  const int t = threadIdx.x;
-  // the two pages of tile j: uniform across the workgroup (scalar loads)
-  const int npg = (kvl + 63) >> 6;
-  const int64_t pg0 = pt[min(2 * j, npg - 1)];
-  const int64_t pg1 = pt[min(2 * j + 1, npg - 1)];
-  {
-    const int key = t >> 2, qt = t & 3;
-    const int kabs = j * kTile + key;
-    const int64_t row = ((key < 64 ? pg0 : pg1) * p.h_kv + hk) * kPage + (kabs & 63);
-    r.kc = (u32x4){0u, 0u, 0u, 0u};
-    r.ksc = 0;
-    if (kabs < kvl) {
-      r.kc = *reinterpret_cast<const u32x4*>(p.k_codes + row * 64 + qt * 16);
-      r.ksc = MX ? (uint32_t)p.k_scales[row * 8 + qt]
-                 : (uint32_t)*reinterpret_cast<const uint16_t*>(p.k_scales + row * 8 + qt * 2);
-    }
-  }
-  {
-    const int d = t >> 2, part = t & 3;
-    const int kbase = j * kTile + part * 32;
-    const int64_t crow = ((part < 2 ? pg0 : pg1) * p.h_kv + hk) * kD + d;   // channel row of the page
-#pragma unroll
-    for (int i = 0; i < TileRegs<PV>::kVWords; ++i) r.v[i] = (u32x4){0u, 0u, 0u, 0u};
-    r.vsc = 0;
-    if (kbase < kvl) {
-      if (PV == kPvFp8) {
-        const uint8_t* src = p.v_codes + crow * kPage + (kbase & 63);
-        r.v[0] = *reinterpret_cast<const u32x4*>(src);
-        r.v[1 % TileRegs<PV>::kVWords] = *reinterpret_cast<const u32x4*>(src + 16);
-        if (kbase + 32 > kvl) {
-          r.v[0] = zero_tail(r.v[0], kvl - kbase);
-          r.v[1 % TileRegs<PV>::kVWords] = zero_tail(r.v[1 % TileRegs<PV>::kVWords], kvl - kbase - 16);
-        }
-      } else if (PV == kPvBf16) {
-        const uint8_t* src = p.v_aux + (crow * kPage + (kbase & 63)) * 2;
-#pragma unroll
-        for (int i = 0; i < TileRegs<PV>::kVWords; ++i) {
-          r.v[i] = *reinterpret_cast<const u32x4*>(src + 16 * i);
-          // keys past kv_len: zero (slots not written may hold any bits)
-          if (kbase + 32 > kvl) r.v[i] = zero_tail(r.v[i], 2 * (kvl - kbase) - 16 * i);
-        }
-      } else {
-        // NVFP4 dequantizes to finite values whatever the bytes, and P is 0 on
-        // keys past kv_len: nothing to clear
-        r.v[0] = *reinterpret_cast<const u32x4*>(p.v_aux + crow * 32 + (kbase & 63) / 2);
-        r.vsc = *reinterpret_cast<const uint16_t*>(p.v_aux + p.num_pages * p.h_kv * kD * 32 + crow * 4 +
-                                                   (kbase & 63) / 16);
-      }
-    }
-  }
-  r.ds = 0;
-  if (t < kTile) {
-    const int kabs = j * kTile + t;
-    if (p.smooth && kabs < kvl)
-      r.ds = p.ds[((t < 64 ? pg0 : pg1) * p.h_q + h) * kPage + (kabs & 63)];
-  }
-}
-
-template <bool MX, int PV>
-__device__ __forceinline__ void store_tile(PrefillSmemT<PV>& sm, const TileRegs<PV>& r, float seed_scale) {
-  const int t = threadIdx.x;
-  if (MX) {
-    const int key = t >> 2, qt = t & 3;
-    *reinterpret_cast<u32x4*>(sm.k + key * 64 + ((qt ^ mx_swz(key)) << 4)) = r.kc;
-    // key -> MFMA row 4*(key/32) + key%4 of 16-key block (key/4)%8
-    const int mrow = 4 * (key >> 5) + (key & 3), mblk = (key >> 2) & 7;
-    sm.k[kMxScaleOff + (mrow * 4 + qt) * 8 + mblk] = (uint8_t)r.ksc;
-  } else {
-    const int key = t >> 2, qt = t & 3;
-    const ScaleSplit s0 = split_e4m3(r.ksc & 0xFFu), s1 = split_e4m3((r.ksc >> 8) & 0xFFu);
-    uint8_t* rowp = sm.k + key * 256;
-    const int sw = k_swz(key);
-    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 0) ^ sw) << 4)) = dequant8(r.kc[0], s0);
-    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 1) ^ sw) << 4)) = dequant8(r.kc[1], s0);
-    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 2) ^ sw) << 4)) = dequant8(r.kc[2], s1);
-    *reinterpret_cast<f16x8*>(rowp + (((4 * qt + 3) ^ sw) << 4)) = dequant8(r.kc[3], s1);
-  }
-  {
-    const int d = t >> 2, part = t & 3;
-    if (PV == kPvFp8) {
-      uint8_t* rowp = sm.v + d * kTile;
-      const int sw = v_swz(d);
-      *reinterpret_cast<u32x4*>(rowp + (((2 * part) ^ sw) << 4)) = r.v[0];
-      *reinterpret_cast<u32x4*>(rowp + (((2 * part + 1) ^ sw) << 4)) = r.v[1 % TileRegs<PV>::kVWords];
-    } else {
-      uint8_t* rowp = sm.v + d * (kTile * 2);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        u32x4 w;
-        if (PV == kPvBf16) {
-          w = r.v[i % TileRegs<PV>::kVWords];
-        } else {   // 8 codes of keys 32 part + 8i .. +7, the scale of their 16-key group
-          const f16x8 hv = dequant8(r.v[0][i], split_e4m3((r.vsc >> (8 * (i >> 1))) & 0xFFu));
-          w = __builtin_bit_cast(u32x4, hv);
-        }
-        *reinterpret_cast<u32x4*>(rowp + (((4 * part + i) ^ (d & 15)) << 4)) = w;
-      }
-    }
-  }
-  // exact: a BF16 value times a power of two stays a BF16 value
-  if (t < kTile) sm.ds[t] = bf16_rne(bf16_to_f32((uint16_t)r.ds) * seed_scale);
-}
-
-// How the compensation 1 Delta_S^T (Sec. 4.3 Eq. 11) enters the score
-// accumulator before the QK product:
-//  kSeedMfma  one BF16 rank-one MFMA per 16-key block (A = the block's Delta_S
-//             in reduction slot 0, B = ones in slot 0); it depends on the keys
-//             only, so its result seeds every query block of the wave;
-//  kSeedInit  the same rank-one matrix loaded directly as the accumulator input
-//             of the first FP16 MFMA (bit-identical: both start the accumulator
-//             at the FP32 value of the BF16 Delta_S);
-//  kSeedNone  no compensation (the unsmoothed "direct" variant);
-//  kSeedElem  the placement the rank-one seed replaces (Sec. 3.2, Fig. 10):
-//             the accumulator starts at zero and Delta_S is added to every
-//             score in FP32 after the QK product, on the softmax path.  Same
-//             values up to the FP32 rounding order.
-enum SeedMode { kSeedNone = 0, kSeedMfma = 1, kSeedInit = 2, kSeedElem = 3 };
-
 template <int SEED, bool MX, int PV>
 __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   __shared__ __attribute__((aligned(16))) PrefillSmemT<PV> smem[2];
-
-  // ---- work item: largest query tiles first (longest-processing-time order)
-  int b, h, rank;
-  {
-    const int bid = blockIdx.x;
-    if (p.xcd_remap) {
-      // block ids are dealt round-robin to the 8 XCDs; give each XCD the query
-      // heads of a fixed subset of KV heads so their K/V tiles share its L2.
-      const int xcd = bid & 7, slot = bid >> 3;
-      const int kvpx = p.h_kv / 8, grp = p.h_q / p.h_kv;
-      const int ipr = kvpx * grp * p.batch;
-      rank = slot / ipr;
-      int r = slot % ipr;
-      const int hk = xcd * kvpx + r % kvpx;
-      r /= kvpx;
-      h = hk * grp + r % grp;
-      b = r / grp;
-    } else {
-      const int per = p.h_q * p.batch;
-      rank = bid / per;
-      const int rem = bid % per;
-      h = rem % p.h_q;
-      b = rem / p.h_q;
-    }
-  }
-  const int qtile = p.n_qtiles - 1 - rank;
-  const int q0 = p.cu_seqlens_q[b];
-  const int nq = p.cu_seqlens_q[b + 1] - q0;
-  const int r0 = qtile * kQRows;
-  if (r0 >= nq) return;
-
-  const int qs = p.q_start[b], kvl = p.kv_len[b];
-  const int grp = p.h_q / p.h_kv, hk = h / grp;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 4, lr = lane & 15;
-  const int last_row = min(r0 + kQRows, nq) - 1;
-  const int j_hi = (qs + last_row) >> 7;
-
-  const float tq = p.q_tscale[b * p.h_q + h], tk = p.k_tscale[b * p.h_kv + hk];
-  const int eqk = ilog2f(tq) + ilog2f(tk);
-  const float lam2 = __builtin_ldexpf(p.lam, eqk);        // lambda * tQ * tK
-  const float seed_scale = __builtin_ldexpf(1.0f, -eqk);  // Delta_S in accumulator units
-
-  const int wrow0 = r0 + wave * (kNB * 16);
-  const bool wave_active = wrow0 < nq;
-  const int wpos_min = qs + wrow0;
-  const int wpos_max = qs + min(wrow0 + kNB * 16, nq) - 1;
-
-  // ---- Q operands (B of S^T = K Q^T).  NVFP4: exact FP16, tensor scale
-  // factored out.  MXFP4: the raw codes of channels 32g .. 32g+31 and their
-  // E8M0 scale (the lane's 32-element block of the scaled FP4 MFMA).
-  f16x8 qop[kNB][4];
-  u32x4 qraw[kNB];
-  int qscale[kNB];
-  int pos[kNB];
-#pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
-    const int row = wrow0 + nb * 16 + lr;
-    pos[nb] = qs + row;
-    const bool valid = row < nq;
-    const int64_t tok = q0 + (valid ? row : 0);
-    const uint8_t* qc = p.q_codes + (tok * p.h_q + h) * 64;
-    const uint8_t* qsc = p.q_scales + (tok * p.h_q + h) * 8;
-    if (MX) {
-      qraw[nb] = valid ? *reinterpret_cast<const u32x4*>(qc + 16 * g) : (u32x4){0u, 0u, 0u, 0u};
-      qscale[nb] = valid ? qsc[g] : 127;
-    } else {
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const uint32_t cw = valid ? *reinterpret_cast<const uint32_t*>(qc + 16 * ks + 4 * g) : 0u;
-        const uint32_t sc = valid ? qsc[2 * ks + (g >> 1)] : 0u;
-        qop[nb][ks] = dequant8(cw, split_e4m3(sc));
-      }
-    }
-  }
-
-  bf16x8 bseed = {};
-  if (lane < 16) bseed[0] = (__bf16)1.0f;
-
-  float m[kNB], l[kNB];
-  f32x4 o[8][kNB];
-#pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
-    m[nb] = -INFINITY;
-    l[nb] = 0.0f;
-#pragma unroll
-    for (int db = 0; db < 8; ++db) o[db][nb] = (f32x4){0.f, 0.f, 0.f, 0.f};
-  }
-
-  const int32_t* pt = p.page_table + (int64_t)b * p.max_pages;
-  {
-    TileRegs<PV> r0r;
-    fetch_tile<MX, PV>(r0r, p, pt, hk, h, j_hi, kvl);
-    store_tile<MX, PV>(smem[j_hi & 1], r0r, seed_scale);
-  }
-  __syncthreads();
-  for (int j = j_hi; j >= 0; --j) {
-    TileRegs<PV> nxt;
-    if (j > 0) fetch_tile<MX, PV>(nxt, p, pt, hk, h, j - 1, kvl);
-    const PrefillSmemT<PV>& sm = smem[j & 1];
-    const int key0 = j * kTile;
-    if (wave_active && key0 <= wpos_max) {
-      const bool need_mask = key0 + kTile - 1 > wpos_min;
-      f32x4 s[8][kNB];
-#pragma unroll
-      for (int mb = 0; mb < 8; ++mb) {
-        f32x4 seed = (f32x4){0.f, 0.f, 0.f, 0.f};
-        if (SEED == kSeedMfma) {
-          bf16x8 aseed = {};
-          aseed[0] = __builtin_bit_cast(__bf16, lane < 16 ? sm.ds[32 * (lr >> 2) + 4 * mb + (lr & 3)]
-                                                          : (uint16_t)0);
-          seed = mfma_bf16(aseed, bseed, seed);
-        } else if (SEED == kSeedInit) {
-          // keys 32g + 4mb .. +3 of the lane's accumulator rows
-          const uint2 d4 = *reinterpret_cast<const uint2*>(&sm.ds[32 * g + 4 * mb]);
-          seed = (f32x4){__uint_as_float(d4.x << 16), __uint_as_float(d4.x & 0xFFFF0000u),
-                         __uint_as_float(d4.y << 16), __uint_as_float(d4.y & 0xFFFF0000u)};
-        }
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = seed;
-      }
-      if (MX) {
-        // one scaled FP4 MFMA per 16x16 block covers all 128 channels
-        const uint64_t ks8 = *reinterpret_cast<const uint64_t*>(sm.k + kMxScaleOff + (lr * 4 + g) * 8);
-#pragma unroll
-        for (int mb = 0; mb < 8; ++mb) {
-          const int krow = 32 * (lr >> 2) + 4 * mb + (lr & 3);
-          const u32x4 kop = *reinterpret_cast<const u32x4*>(sm.k + krow * 64 + ((g ^ mx_swz(krow)) << 4));
-          const int sk = (int)((ks8 >> (8 * mb)) & 0xFFu);
-#pragma unroll
-          for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_fp4(kop, qraw[nb], s[mb][nb], sk, qscale[nb]);
-        }
-      } else {
-#pragma unroll
-        for (int half = 0; half < 2; ++half)
-#pragma unroll
-          for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-            for (int mb = 4 * half; mb < 4 * half + 4; ++mb) {
-              const int krow = 32 * (lr >> 2) + 4 * mb + (lr & 3);
-              const f16x8 kop = *reinterpret_cast<const f16x8*>(sm.k + krow * 256 + (((4 * ks + g) ^ lr) << 4));
-#pragma unroll
-              for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_f16(kop, qop[nb][ks], s[mb][nb]);
-            }
-          }
-      }
-      if (SEED == kSeedElem) {
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb)
-#pragma unroll
-          for (int mb = 0; mb < 8; ++mb) {
-            const uint2 d4 = *reinterpret_cast<const uint2*>(&sm.ds[32 * g + 4 * mb]);
-            s[mb][nb][0] += __uint_as_float(d4.x << 16);
-            s[mb][nb][1] += __uint_as_float(d4.x & 0xFFFF0000u);
-            s[mb][nb][2] += __uint_as_float(d4.y << 16);
-            s[mb][nb][3] += __uint_as_float(d4.y & 0xFFFF0000u);
-          }
-      }
-      if (need_mask) {
-#pragma unroll
-        for (int mb = 0; mb < 8; ++mb)
-#pragma unroll
-          for (int nb = 0; nb < kNB; ++nb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              if (key0 + 32 * g + 4 * mb + i > pos[nb]) s[mb][nb][i] = -INFINITY;
-      }
-      // log2 of the fixed factor the P quantizer applies: 448 (FP8), 1 (BF16),
-      // 2688 = 6 * 448 (NVFP4: the largest P, 1, maps to the top E2M1 code
-      // under the largest E4M3 scale)
-      constexpr float kLog2PScale = PV == kPvFp8 ? kLog2_448 : (PV == kPvBf16 ? 0.0f : 11.392317422778760f);
-      i32x8 pb[kNB];
-      f16x8 ph[kNB][4];   // BF16 (bit pattern) or dequantized NVFP4 P, keys 32g + 8kk .. +7
-      float alpha[kNB];
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int mb = 0; mb < 8; ++mb)
-          mx = fmaxf(fmaxf(mx, fmaxf(s[mb][nb][0], s[mb][nb][1])), fmaxf(s[mb][nb][2], s[mb][nb][3]));
-        mx = wave_max16(mx);
-        const float mnew = fmaxf(m[nb], mx);
-        const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
-        alpha[nb] = (m[nb] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m[nb] - muse) * lam2);
-        m[nb] = mnew;
-        const float bias = __builtin_fmaf(-muse, lam2, kLog2PScale);
-        float ps = 0.0f;
-        float ev[8][4];
-#pragma unroll
-        for (int mb = 0; mb < 8; ++mb) {
-          float e[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][nb][i], lam2, bias));
-          ps += (e[0] + e[1]) + (e[2] + e[3]);
-          if (PV == kPvFp8) {
-            pb[nb][mb] = (int)pack_fp8x4(e[0], e[1], e[2], e[3]);
-          } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) ev[mb][i] = e[i];
-          }
-        }
-        l[nb] = alpha[nb] * l[nb] + ps;
-        if (PV == kPvBf16) {
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk) {
-            bf16x8 b;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              b[i] = (__bf16)ev[2 * kk][i];
-              b[4 + i] = (__bf16)ev[2 * kk + 1][i];
-            }
-            ph[nb][kk] = __builtin_bit_cast(f16x8, b);
-          }
-        } else if (PV == kPvNvfp4) {
-          // the lane's 32 keys are two 16-key groups: keys 32g .. +15 (mb 0..3)
-          // and 32g + 16 .. +31 (mb 4..7); scale E4M3(amax / 6), codes E2M1(P'/scale)
-#pragma unroll
-          for (int half = 0; half < 2; ++half) {
-            float amax = 0.0f;
-#pragma unroll
-            for (int mb = 4 * half; mb < 4 * half + 4; ++mb)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) amax = fmaxf(amax, ev[mb][i]);
-            const uint32_t sc = fp8_sat_pair(0u, div_by_scale(amax, 6.0f, kRcp6), 0.0f, false) & 0xFFu;
-            const float sd = e4m3_value(sc);
-            uint32_t cw[2] = {0u, 0u};
-            if (sd > 0.0f) {
-              const float r = __fdiv_rn(1.0f, sd);
-#pragma unroll
-              for (int w = 0; w < 2; ++w)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                  const int mb = 4 * half + 2 * w + (j >> 1), i0 = 2 * (j & 1);
-                  cw[w] = fp4_pair(cw[w], div_by_scale(ev[mb][i0], sd, r), div_by_scale(ev[mb][i0 + 1], sd, r),
-                                   1.0f, j);
-                }
-            }
-            const ScaleSplit sp = split_e4m3(sc);
-            ph[nb][2 * half] = dequant8(cw[0], sp);
-            ph[nb][2 * half + 1] = dequant8(cw[1], sp);
-          }
-        }
-      }
-      bool moved = false;
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) moved |= alpha[nb] != 1.0f;
-      if (__builtin_amdgcn_ballot_w64(moved) != 0) {
-#pragma unroll
-        for (int db = 0; db < 8; ++db)
-#pragma unroll
-          for (int nb = 0; nb < kNB; ++nb) o[db][nb] *= alpha[nb];
-      }
-      if (PV == kPvFp8) {
-#pragma unroll
-        for (int db = 0; db < 8; ++db) {
-          const int d = 16 * db + lr;
-          const uint8_t* vr = sm.v + d * kTile;
-          const int sw = v_swz(d);
-          const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((2 * g) ^ sw) << 4));
-          const u32x4 vb = *reinterpret_cast<const u32x4*>(vr + (((2 * g + 1) ^ sw) << 4));
-          const i32x8 vop = {(int)va[0], (int)va[1], (int)va[2], (int)va[3],
-                             (int)vb[0], (int)vb[1], (int)vb[2], (int)vb[3]};
-#pragma unroll
-          for (int nb = 0; nb < kNB; ++nb) o[db][nb] = mfma_fp8(vop, pb[nb], o[db][nb]);
-        }
-      } else {
-        // four 32-key MFMAs per channel block: MFMA kk reduces keys 32g + 8kk .. +7
-        // of every lane group g, so A (V row chunk 4g + kk) and B (the lane's own
-        // P values) pair the same keys
-#pragma unroll
-        for (int db = 0; db < 8; ++db) {
-          const uint8_t* vr = sm.v + (16 * db + lr) * (kTile * 2);
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk) {
-            const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((4 * g + kk) ^ lr) << 4));
-#pragma unroll
-            for (int nb = 0; nb < kNB; ++nb) {
-              if (PV == kPvBf16)
-                o[db][nb] = mfma_bf16(__builtin_bit_cast(bf16x8, va), __builtin_bit_cast(bf16x8, ph[nb][kk]),
-                                      o[db][nb]);
-              else
-                o[db][nb] = mfma_f16(__builtin_bit_cast(f16x8, va), ph[nb][kk], o[db][nb]);
-            }
-          }
-        }
-      }
-    }
-    if (j > 0) store_tile<MX, PV>(smem[(j - 1) & 1], nxt, seed_scale);
-    __syncthreads();
-  }
-
-  if (!wave_active) return;
-  // ---- epilogue: out = O / (448 l), BF16
-#pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
-    const float lt = wave_sum16(l[nb]);
-    const int row = wrow0 + nb * 16 + lr;
-    if (row < nq) {
-      uint16_t* dst = p.out + ((int64_t)(q0 + row) * p.h_q + h) * kD;
-      const float inv = __frcp_rn(lt);
-#pragma unroll
-      for (int db = 0; db < 8; ++db) {
-        const uint32_t lo = (uint32_t)bf16_rne(o[db][nb][0] * inv) |
-                            ((uint32_t)bf16_rne(o[db][nb][1] * inv) << 16);
-        const uint32_t hi = (uint32_t)bf16_rne(o[db][nb][2] * inv) |
-                            ((uint32_t)bf16_rne(o[db][nb][3] * inv) << 16);
-        *reinterpret_cast<uint2*>(dst + 16 * db + 4 * g) = make_uint2(lo, hi);
-      }
-    }
-  }
+  prefill_item<SEED, MX, PV>(p, blockIdx.x, smem);
 }
 
 }  // namespace

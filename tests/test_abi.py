@@ -133,3 +133,26 @@ def test_convert_validation(mp):
     assert mp.lib().mpfa_convert(4, None, 0, None, None) == 1
     assert mp.lib().mpfa_convert(-1, None, 0, None, None) == 1
     assert mp.lib().mpfa_convert(0, None, 5, None, None) == 1
+
+
+def test_mixed_step_validation(mp):
+    """Host validation of the fused step: workspace size, flag consistency,
+    unsupported prefill placements; nothing is launched on these paths."""
+    n = C.c_size_t(0)
+    assert mp.lib().mpfa_mixed_workspace_size(2, 32, 8, 3, C.byref(n)) == 0
+    states = 2 * 32 * 3 * 130 * 4
+    assert n.value == (states + 255) // 256 * 256 + 2 * 8 * 4
+    assert mp.lib().mpfa_mixed_workspace_size(2, 32, 0, 3, C.byref(n)) == 1
+    pa = _prefill_args(mp, h_q=32, h_kv=8)
+    da = _decode_args(mp, max_partitions=3)
+    # smoothing differs between the parts
+    pa.flags, da.flags = 1, 0
+    assert mp.lib().mpfa_mixed_step(C.byref(pa), C.byref(da), 0x1000, 1 << 30, None) == 1
+    # placements the fused kernel does not run
+    for f in (1 | 8, 1 | 32, 1 | 64):
+        pa.flags, da.flags = f, 1
+        assert mp.lib().mpfa_mixed_step(C.byref(pa), C.byref(da), 0x1000, 1 << 30, None) == 2
+    # workspace too small for states + counters
+    pa.flags, da.flags = 1, 1
+    assert mp.lib().mpfa_mixed_step(C.byref(pa), C.byref(da), 0x1000, states, None) == 3
+    assert mp.lib().mpfa_mixed_step(None, C.byref(da), 0x1000, 1 << 30, None) == 1

@@ -200,6 +200,22 @@ def test_mixed_step_qwen(orc, mp, W):
     print("mixed step: launched", flush=True)
     got_pre = H.bits(out_pre)
     got_dec = H.bits(out_dec)
+    # --- the same step as one fused launch: identical bytes, twice (counters reset)
+    wsm = torch.zeros(mp.mixed_workspace_size(dec.batch, h_q, h_kv, maxp) // 4, dtype=torch.float32,
+                      device=dev)
+    for rep in range(2):
+        fo_pre = torch.full_like(out_pre, float("nan"))
+        fo_dec = torch.full_like(out_dec, float("nan"))
+        mp.mixed_step(dict(qq=qq_pre, cache=cache, stats=st_pre, cu_seqlens_q=d(np.array([0, chunk], np.int32)),
+                           q_start=d(np.array([prefix], np.int32)), kv_len=d(np.array([total], np.int32)),
+                           page_table=d(pt_pre), out=fo_pre, max_seqlen_q=chunk),
+                      dict(qq=qq_dec, cache=cache, stats=st_dec, kv_len=d(lens.astype(np.int32)),
+                           page_table=d(pt_dec), out=fo_dec, partition_tokens=part, max_partitions=maxp),
+                      wsm, mp.SMOOTH)
+        torch.cuda.synchronize()
+        assert np.array_equal(H.bits(fo_pre), got_pre), f"fused prefill differs (call {rep})"
+        assert np.array_equal(H.bits(fo_dec), got_dec), f"fused decode differs (call {rep})"
+    print("mixed step: fused launch identical", flush=True)
     # --- oracle: the request (prefix statistics frozen, chunk appended), sampled rows
     qp, kp, vp = W.gen_qkv(pre.seed, [prefix], h_q, h_kv, True, dev)
     npg = (total + 63) // 64
