@@ -84,6 +84,8 @@ def parse():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-direct", action="store_true", help="skip the unsmoothed prefill variant")
     ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant runs")
+    ap.add_argument("--no-mixed", action="store_true",
+                    help="skip the mixed serving step (separate launches vs one fused launch)")
     ap.add_argument("--no-precision", action="store_true",
                     help="skip the BF16 / NVFP4 PV precision-assignment runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -236,6 +238,79 @@ def error_vs_fp64(np, out, ref):
         den += float((ref["o"][h] ** 2).sum())
         mx = max(mx, float(np.abs(d).max()))
     return {"rel_l2": math.sqrt(num / den), "max_abs": mx}
+
+
+def setup_mixed(torch, np, mp, W):
+    """The mixed serving step (Qwen shapes): a 32768-token chunk at position
+    65536 over its cached prefix, and 64 decode sequences with contexts
+    U[8192, 131072] whose caches are written first; then the step's own
+    quantization (chunk and new tokens).  Returns the launch arguments."""
+    pre, dec = W.mixed_step()
+    dev = "cuda"
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    h_q, h_kv = pre.h_q, pre.h_kv
+    prefix, chunk = pre.q_start[0], pre.seqlens[0]
+    total = prefix + chunk
+    pt_pre, np_pre = W.make_pages(pre.seed, [total])
+    pt_dec, np_dec = W.make_pages(dec.seed, dec.kv_len)
+    pt_dec = pt_dec + np_pre
+    cache = mp.PagedCache(np_pre + np_dec, h_q, h_kv, dev)
+    st_pre = mp.SeqStats(1, h_q, h_kv, dev)
+    qp, kp, vp = W.gen_qkv(pre.seed, [prefix], h_q, h_kv, True, dev)
+    mp.quantize_qk(qp, kp, vp, d(np.array([0, prefix], np.int32)), d(W.slots_for(pt_pre, 0, range(prefix))),
+                   cache, st_pre, mp.QuantQ(prefix, 1, h_q, dev), mp.SMOOTH | mp.COMPUTE_STATS, prefix)
+    del qp, kp, vp
+    lens = np.asarray(dec.kv_len)
+    ctx = [int(n) - 1 for n in lens]
+    st_dec = mp.SeqStats(dec.batch, h_q, h_kv, dev)
+    for b0 in range(0, dec.batch, 8):   # contexts in batches of 8 sequences
+        ids = list(range(b0, min(b0 + 8, dec.batch)))
+        q, k, v = W.gen_qkv(dec.seed, [ctx[b] for b in ids], h_q, h_kv, True, dev, seq_ids=ids)
+        cu = np.concatenate([[0], np.cumsum([ctx[b] for b in ids])]).astype(np.int32)
+        slots = np.concatenate([W.slots_for(pt_dec, b, range(ctx[b])) for b in ids])
+        sb = mp.SeqStats(len(ids), h_q, h_kv, dev)
+        mp.quantize_qk(q, k, v, d(cu), d(slots), cache, sb, mp.QuantQ(int(cu[-1]), len(ids), h_q, dev),
+                       mp.SMOOTH | mp.COMPUTE_STATS, max(ctx[b] for b in ids))
+        for i, b in enumerate(ids):
+            st_dec.q_mean[b].copy_(sb.q_mean[i])
+            st_dec.k_mean[b].copy_(sb.k_mean[i])
+            st_dec.k_tscale[b].copy_(sb.k_tscale[i])
+        del q, k, v
+    qc, kc, vc = W.gen_qkv(pre.seed, [chunk], h_q, h_kv, True, dev, tok_offsets=[prefix])
+    qq_pre = mp.QuantQ(chunk, 1, h_q, dev)
+    mp.quantize_qk(qc, kc, vc, d(np.array([0, chunk], np.int32)), d(W.slots_for(pt_pre, 0, range(prefix, total))),
+                   cache, st_pre, qq_pre, mp.SMOOTH, chunk)
+    qn, kn, vn = W.gen_qkv(dec.seed, [1] * dec.batch, h_q, h_kv, True, dev, tok_offsets=ctx)
+    qq_dec = mp.QuantQ(dec.batch, dec.batch, h_q, dev)
+    slots1 = np.array([W.slots_for(pt_dec, b, [ctx[b]])[0] for b in range(dec.batch)], np.int64)
+    mp.quantize_qk(qn, kn, vn, d(np.arange(dec.batch + 1, dtype=np.int32)), d(slots1), cache, st_dec, qq_dec,
+                   mp.SMOOTH, 1)
+    part = mp.decode_choose_partition(lens, h_kv, torch.cuda.get_device_properties(0).multi_processor_count)
+    maxp = max(math.ceil(n / part) for n in lens)
+    pre_args = dict(qq=qq_pre, cache=cache, stats=st_pre, cu_seqlens_q=d(np.array([0, chunk], np.int32)),
+                    q_start=d(np.array([prefix], np.int32)), kv_len=d(np.array([total], np.int32)),
+                    page_table=d(pt_pre), out=torch.empty((chunk, h_q, 128), dtype=torch.bfloat16, device=dev),
+                    max_seqlen_q=chunk)
+    dec_args = dict(qq=qq_dec, cache=cache, stats=st_dec, kv_len=d(lens.astype(np.int32)), page_table=d(pt_dec),
+                    out=torch.empty((dec.batch, h_q, 128), dtype=torch.bfloat16, device=dev),
+                    partition_tokens=part, max_partitions=maxp)
+    ws = torch.empty(mp.decode_workspace_size(dec.batch, h_q, maxp) // 4, dtype=torch.float32, device=dev)
+    wsm = torch.zeros(mp.mixed_workspace_size(dec.batch, h_q, h_kv, maxp) // 4, dtype=torch.float32, device=dev)
+    pairs = sum((prefix + i + 1) for i in range(chunk)) * h_q
+    keys = int(lens.sum())
+    return dict(pre=pre_args, dec=dec_args, ws=ws, wsm=wsm, pairs=pairs, keys=keys, part=part)
+
+
+def run_mixed_separate(mp, mx):
+    a, b = mx["pre"], mx["dec"]
+    mp.prefill(a["qq"], a["cache"], a["stats"], a["cu_seqlens_q"], a["q_start"], a["kv_len"], a["page_table"],
+               a["out"], a["max_seqlen_q"], mp.SMOOTH)
+    mp.decode_paged(b["qq"], b["cache"], b["stats"], b["kv_len"], b["page_table"], b["out"],
+                    b["partition_tokens"], b["max_partitions"], mx["ws"], mp.SMOOTH)
+
+
+def run_mixed_fused(mp, mx):
+    mp.mixed_step(mx["pre"], mx["dec"], mx["wsm"], mp.SMOOTH)
 
 
 def quant_bytes(wl, seq):
@@ -490,6 +565,28 @@ def main():
                                    "frac_hbm": mx_bytes / (mx_ms * 1e-3) / PEAK_HBM,
                                    "bytes": mx_bytes}
             del sx
+
+    if not args.no_mixed:
+        log("mixed serving step: setup ...")
+        mx = setup_mixed(torch, np, mp, W)
+        res_m = {}
+        for name, fn in (("separate_ms", run_mixed_separate), ("fused_ms", run_mixed_fused)):
+            for _ in range(max(args.warmup, 1)):
+                fn(mp, mx)
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(args.steps):
+                with Timer(torch) as t:
+                    fn(mp, mx)
+                ts.append(t)
+            torch.cuda.synchronize()
+            res_m[name] = sum(t.ms() for t in ts) / args.steps
+        res_m["workload"] = ("qwen3-14b-shaped: 32768-token chunk at position 65536 + 64 decode sequences, "
+                             f"contexts U[8192,131072] ({mx['keys']} keys, partition {mx['part']})")
+        res_m["attention_tflops_fused"] = 4.0 * 128 * mx["pairs"] / (res_m["fused_ms"] * 1e-3) / 1e12
+        res["mixed_step"] = res_m
+        del mx
+        torch.cuda.empty_cache()
 
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")

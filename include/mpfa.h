@@ -266,9 +266,9 @@ mpfa_status mpfa_decode_paged(const mpfa_decode_args* args, void* workspace, siz
 /* ------------------------------------------------------------------------ */
 /*
  * Runs the causal prefill described by `prefill` and the split-KV decode
- * described by `decode` in a single kernel launch, merge included: prefill
- * query tiles (matrix-bound) and decode partitions (HBM-bound) are
- * interleaved over the grid so both resources work in the same interval.
+ * described by `decode` in a single kernel launch, merge included (the last
+ * partition of each (sequence, KV head) merges its query heads): decode
+ * partitions first, then the prefill query tiles, in one grid.
  * Results are bit-identical to mpfa_prefill followed by mpfa_decode_paged
  * with the same arguments.  Both parts must use the same MPFA_SMOOTH /
  * MPFA_MXFP4 setting (else MPFA_ERR_INVALID); the prefill flags may not

@@ -271,11 +271,16 @@ mpfa_status mpfa_mixed_step(const mpfa_prefill_args* prefill, const mpfa_decode_
   mpfa_decode_workspace_size(decode->batch, decode->h_q, decode->max_partitions, &states);
   m.counters = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(workspace) + mixed_counter_offset(states));
   const int64_t n_pre = (int64_t)m.pre.n_qtiles * m.pre.h_q * m.pre.batch;
-  const int64_t n_dec = ((int64_t)m.dec.batch * m.dec.h_kv * m.dec.max_partitions + 7) / 8;
-  if (n_pre + n_dec > INT32_MAX) return MPFA_ERR_INVALID;
+  const int64_t n_items = (int64_t)m.dec.batch * m.dec.h_kv * m.dec.max_partitions;
+  const int64_t n_rounds = (n_items + 63) / 64;                  // decode rounds of 8 x 8 items
+  const int64_t pre_rounds = (n_pre + 7) / 8;
+  if (n_pre + 64 * n_rounds + 8 > INT32_MAX) return MPFA_ERR_INVALID;
   m.n_pre_blocks = (int)n_pre;
-  m.n_dec_blocks = (int)n_dec;
-  m.stride = n_dec > 0 ? (int)((n_pre + n_dec) / n_dec) : (int)(n_pre + n_dec + 1);
+  m.n_dec_rounds = (int)n_rounds;
+  // decode rounds first, back to back, then the prefill items (see mixed.hip)
+  m.stride = 1;
+  m.first = 0;
+  m.n_blocks = (int)(8 * (pre_rounds + n_rounds));
   return mpfa::launch_mixed(m, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
                                                                                     : MPFA_ERR_HIP;
 }

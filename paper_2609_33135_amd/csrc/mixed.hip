@@ -1,17 +1,21 @@
 // mixed.hip -- one launch for a serving step that mixes a causal prefill chunk
 // and split-KV decode (Sec. 7.3: prefill and decode requests served together).
 //
-// The prefill work items (query head, 256-row query tile; compute-bound on the
-// matrix cores) and groups of eight decode work items (sequence, KV head,
-// partition; HBM-bound) share one grid.  Decode groups are spread evenly
-// through the dispatch order, so while most compute units run prefill tiles
-// the others stream KV pages, and both resources stay busy in the same
-// interval instead of one launch after the other.  Each decode partition
-// counts itself in a per-(sequence, KV head) counter when its state is
-// written; the last one merges the group's query heads (log-sum-exp, the same
-// arithmetic as the separate merge kernel) and resets the counter, so the
-// step needs no second launch.  A workgroup is 512 threads with 128 KB of
-// LDS: two prefill tile buffers, or eight 16 KB decode V slabs.
+// The prefill work items (query head, 256-row query tile; matrix-bound) and
+// groups of eight decode work items (sequence, KV head, partition; HBM-bound)
+// share one grid.  Each decode partition counts itself in a per-(sequence, KV
+// head) counter when its state is written; the last one merges the group's
+// query heads (log-sum-exp, the same arithmetic as the separate merge kernel)
+// and resets the counter, so the step needs no second launch.  A workgroup is
+// 512 threads with 128 KB of LDS: two prefill tile buffers, or eight 16 KB
+// decode V slabs.
+//
+// Placement: a prefill workgroup holds a whole compute unit (its LDS and all
+// of its registers), so prefill and decode cannot share a unit at the same
+// time; decode rounds spread through the prefill only take unit time from it
+// (measured slower than two launches).  The host therefore places the decode
+// rounds first: they stream the KV pages at full bandwidth on every unit, then
+// the prefill tiles follow in their largest-first order.
 #include "decode_body.h"
 #include "prefill_body.h"
 
@@ -22,23 +26,32 @@ namespace {
 constexpr int kMixedLds = 8 * kVBytes;
 static_assert(sizeof(PrefillSmemT<kPvFp8>) * 2 <= kMixedLds, "prefill tiles must fit the mixed LDS");
 
-// Block i of the grid: the decode groups sit at positions stride-1, 2*stride-1,
-// ... (stride = total / decode groups), the prefill items fill the rest in
-// their own order (largest query tiles first).
+// Blocks are dealt to the 8 XCDs round-robin, so the grid is laid out in rounds
+// of 8 consecutive blocks.  Decode rounds (8 groups of 8 decode work items)
+// sit at round indices first, first + stride, ...; prefill items fill the
+// other rounds in their own order (largest query tiles first).  Whole rounds keep
+// every prefill item on the XCD its index selects (index = block - 8 * decode
+// rounds before it, the same residue mod 8), so the KV-head-per-XCD placement
+// of the prefill items holds as in the separate launch.
 template <bool SMOOTH, bool MX>
 __global__ __launch_bounds__(512, 1) void mixed_kernel(MixedParams m) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[kMixedLds];
-  const int i = blockIdx.x;
-  const int dec_before = min((i + 1) / m.stride, m.n_dec_blocks);
-  const bool is_dec = m.n_dec_blocks > 0 && (i + 1) % m.stride == 0 && (i + 1) / m.stride <= m.n_dec_blocks;
+  const int i = blockIdx.x, r = i >> 3;
+  // decode round k sits at round first + k * stride (k < n_dec_rounds)
+  const int rel = r - m.first;
+  const bool is_dec = rel >= 0 && rel % m.stride == 0 && rel / m.stride < m.n_dec_rounds;
+  const int dec_before = rel < 0 ? 0 : min(rel / m.stride + 1, m.n_dec_rounds);   // rounds <= r
   if (!is_dec) {
-    prefill_item<SMOOTH ? kSeedMfma : kSeedNone, MX, kPvFp8>(m.pre, i - dec_before,
+    const int bid = i - 8 * dec_before;
+    if (bid >= m.n_pre_blocks) return;
+    prefill_item<SMOOTH ? kSeedMfma : kSeedNone, MX, kPvFp8>(m.pre, bid,
                                                              reinterpret_cast<PrefillSmemT<kPvFp8>*>(lds));
     return;
   }
-  // decode group k: wave w takes item 8k + w = ((b * h_kv + hk) * max_partitions + part)
+  // decode group (round, lane of the round): wave w takes item 8 * group + w =
+  // ((b * h_kv + hk) * max_partitions + part)
   const int wave = threadIdx.x >> 6;
-  const int item = (dec_before - 1) * 8 + wave;
+  const int item = ((dec_before - 1) * 8 + (i & 7)) * 8 + wave;
   const DecodeParams& p = m.dec;
   const int part = item % p.max_partitions;
   const int hk = (item / p.max_partitions) % p.h_kv;
@@ -50,7 +63,7 @@ __global__ __launch_bounds__(512, 1) void mixed_kernel(MixedParams m) {
 }  // namespace
 
 hipError_t launch_mixed(const MixedParams& m, hipStream_t stream) {
-  const unsigned blocks = (unsigned)(m.n_pre_blocks + m.n_dec_blocks);
+  const unsigned blocks = (unsigned)m.n_blocks;
   if (blocks == 0) return hipSuccess;
   const dim3 grid(blocks), block(512);
   if (m.pre.mx) {

@@ -86,8 +86,10 @@ struct MixedParams {
   PrefillParams pre;
   DecodeParams dec;
   int n_pre_blocks;   // prefill work items (query tiles x heads x sequences)
-  int n_dec_blocks;   // groups of 8 decode work items
-  int stride;         // a decode group every `stride` blocks
+  int n_dec_rounds;   // rounds of 8 decode groups (a group is 8 decode work items)
+  int first;          // round index of the first decode round
+  int stride;         // rounds of 8 blocks from one decode round to the next
+  int n_blocks;       // grid size
   uint32_t* counters; // [dec.batch][dec.h_kv] partition counters, zero between calls
 };
 
