@@ -33,8 +33,10 @@ PEAK_HBM = 8.0e12         # bytes/s
 # reported only while the kernel's sources hash to the value recorded with it.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.txt")
 KERNEL_SOURCES = {
-    "prefill_kernel": ["csrc/prefill.hip", "csrc/mpfa_device.h", "csrc/mpfa_internal.h", "csrc/api.cpp"],
-    "decode_kernel": ["csrc/decode.hip", "csrc/mpfa_device.h", "csrc/mpfa_internal.h", "csrc/api.cpp"],
+    "prefill_kernel": ["csrc/prefill.hip", "csrc/prefill_body.h", "csrc/mpfa_device.h", "csrc/mpfa_internal.h",
+                       "csrc/api.cpp"],
+    "decode_kernel": ["csrc/decode.hip", "csrc/decode_body.h", "csrc/mpfa_device.h", "csrc/mpfa_internal.h",
+                      "csrc/api.cpp"],
 }
 
 
