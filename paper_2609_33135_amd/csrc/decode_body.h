@@ -27,15 +27,38 @@ typedef __attribute__((address_space(1))) void* global_ptr_t;
 // channel 16 db + lane%16, keys 32 (lane/16) + 16 hf .. +15.
 // Merge of the partition states of one (sequence, query head) for output
 // channel d: log-sum-exp over the partitions in order, then O / L, BF16.
+// The loads of 16 partitions are issued together; the accumulation order stays
+// partition 0, 1, 2, ...
 __device__ __forceinline__ float merge_channel(const DecodeParams& p, int b, int h, int d, int np) {
+  constexpr int kBatch = 16;
   const float* st = p.ws + ((int64_t)b * p.h_q + h) * p.max_partitions * (kD + 2);
   float M = -INFINITY;
-  for (int q = 0; q < np; ++q) M = fmaxf(M, st[q * (kD + 2)]);
+  for (int q0 = 0; q0 < np; q0 += kBatch) {
+    float mv[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) mv[j] = q0 + j < np ? st[(q0 + j) * (kD + 2)] : -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) M = fmaxf(M, mv[j]);
+  }
   float L = 0.0f, O = 0.0f;
-  for (int q = 0; q < np; ++q) {
-    const float f = __builtin_amdgcn_exp2f(st[q * (kD + 2)] - M);
-    L = __builtin_fmaf(f, st[q * (kD + 2) + 1], L);
-    O = __builtin_fmaf(f, st[q * (kD + 2) + 2 + d], O);
+  for (int q0 = 0; q0 < np; q0 += kBatch) {
+    float mv[kBatch], lv[kBatch], ov[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const bool in = q0 + j < np;
+      const float* sq = st + (q0 + j) * (kD + 2);
+      mv[j] = in ? sq[0] : 0.0f;
+      lv[j] = in ? sq[1] : 0.0f;
+      ov[j] = in ? sq[2 + d] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (q0 + j < np) {
+        const float f = __builtin_amdgcn_exp2f(mv[j] - M);
+        L = __builtin_fmaf(f, lv[j], L);
+        O = __builtin_fmaf(f, ov[j], O);
+      }
+    }
   }
   return np > 0 ? __fdiv_rn(O, L) : 0.0f;
 }
