@@ -295,8 +295,12 @@ mpfa_status mpfa_mixed_step(const mpfa_prefill_args* prefill, const mpfa_decode_
  * kept), fmt 1 = FP32 -> E2M1 (RNE, saturating at 6, sign kept, one code per
  * output byte), both written out from the format definitions; fmt 2 and 3 =
  * the same two conversions through the gfx950 hardware converters, as the
- * quantization pass uses them (must give identical bytes).  x and out are
- * device pointers of n elements; MPFA_ERR_INVALID for another fmt. */
+ * quantization pass uses them (must give identical bytes); 0x100 + c (c =
+ * 1..126, a positive E4M3 code) = the E2M1 code of x / e4m3(c) exactly as the
+ * NVFP4 quantizer forms it (the correctly rounded quotient, then E2M1);
+ * 0x200 + b (b = 1..254) = the E2M1 code of x / 2^(b - 127) as the MXFP4
+ * quantizer forms it.  x and out are device pointers of n elements;
+ * MPFA_ERR_INVALID for another fmt. */
 mpfa_status mpfa_convert(int32_t fmt, const float* x, int64_t n, uint8_t* out,
                          mpfa_stream_t stream);
 

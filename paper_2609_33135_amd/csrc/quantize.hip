@@ -526,11 +526,19 @@ __global__ void convert_kernel(int fmt, const float* x, int64_t n, uint8_t* out)
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   uint32_t c;
-  switch (fmt) {
-    case 0: c = e4m3_rne_sat(x[i]); break;
-    case 1: c = e2m1_rne_sat(x[i]); break;
-    case 2: c = fp8_sat_pair(0u, x[i], 0.0f, false) & 0xFFu; break;
-    default: c = fp4_pair(0u, x[i], 0.0f, 1.0f, 0) & 0xFu; break;
+  if (fmt >= 0x200) {   // MXFP4 element: x / 2^e, e = (fmt & 0xFF) - 127 >= -126
+    c = fp4_pair(0u, x[i], 0.0f, __builtin_ldexpf(1.0f, (fmt & 0xFF) - 127), 0) & 0xFu;
+  } else if (fmt >= 0x100) {   // NVFP4 element: x / e4m3_value(fmt & 0xFF), the quantizer's division
+    const float s = e4m3_value(fmt & 0xFF), r = __fdiv_rn(1.0f, s);
+    if (__builtin_fabsf(x[i]) * r < 0x1p100f) c = fp4_pair(0u, div_by_scale(x[i], s, r), 0.0f, 1.0f, 0) & 0xFu;
+    else c = e2m1_rne_sat(__fdiv_rn(x[i], s));   // the quantizer's fallback near the FP32 range
+  } else {
+    switch (fmt) {
+      case 0: c = e4m3_rne_sat(x[i]); break;
+      case 1: c = e2m1_rne_sat(x[i]); break;
+      case 2: c = fp8_sat_pair(0u, x[i], 0.0f, false) & 0xFFu; break;
+      default: c = fp4_pair(0u, x[i], 0.0f, 1.0f, 0) & 0xFu; break;
+    }
   }
   out[i] = (uint8_t)c;
 }

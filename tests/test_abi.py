@@ -130,8 +130,8 @@ def test_quantize_validation(mp):
 
 
 def test_convert_validation(mp):
-    assert mp.lib().mpfa_convert(4, None, 0, None, None) == 1
-    assert mp.lib().mpfa_convert(-1, None, 0, None, None) == 1
+    for bad in (4, -1, 0x100, 0x17F, 0x200, 0x2FF, 0x300):
+        assert mp.lib().mpfa_convert(bad, None, 0, None, None) == 1, bad
     assert mp.lib().mpfa_convert(0, None, 5, None, None) == 1
 
 

@@ -200,3 +200,45 @@ def test_quantize_pv_copies(orc, mp, pv):
     assert got.shape == ref.shape
     bad = np.nonzero(got != ref)[0]
     assert bad.size == 0, (bad[:5], got[bad[:5]], ref[bad[:5]])
+
+
+def test_quantizer_division_sweep(orc, mp):
+    """The NVFP4 quantizer's element path (correctly rounded x / scale from the
+    rounded reciprocal and one residual step, then the FP4 converter) for all
+    126 positive E4M3 scales, and the MXFP4 power-of-two path for a spread of
+    exponents, against the oracle's IEEE FP32 division and E2M1 encoder, over a
+    stride of all FP32 bit patterns plus the neighbourhoods of every decision
+    threshold times the scale."""
+    print("case: quantizer division sweep", flush=True)
+    pats = np.arange(0, 1 << 32, 9973, dtype=np.uint64).astype(np.uint32)
+    base = pats.view(np.float32)
+    base = base[np.isfinite(base)]
+    xd_base = torch.from_numpy(base).cuda()
+    out = torch.empty(base.size, dtype=torch.uint8, device="cuda")
+    thresholds = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 6.0], np.float32)
+    for c in range(1, 0x7F):
+        s = np.float32(orc.e4m3_value(c))
+        mp.convert(0x100 + c, xd_base, out)
+        torch.cuda.synchronize()
+        with np.errstate(over="ignore"):   # quotients past FP32 saturate like +-inf
+            ref = orc.e2m1_encode(base / s)
+        bad = np.nonzero(out.cpu().numpy() != ref)[0]
+        assert bad.size == 0, (c, base[bad[:4]])
+        # dense neighbourhoods of threshold * scale (the rounding decisions)
+        cen = (thresholds * s).astype(np.float32).view(np.uint32).astype(np.int64)
+        nb = (cen[:, None] + np.arange(-300, 301)[None, :]).reshape(-1)
+        nb = nb[(nb > 0) & (nb < 0x7F800000)].astype(np.uint32)
+        x = np.concatenate([nb, nb | np.uint32(0x80000000)]).view(np.float32)
+        o2 = torch.empty(x.size, dtype=torch.uint8, device="cuda")
+        mp.convert(0x100 + c, torch.from_numpy(x).cuda(), o2)
+        torch.cuda.synchronize()
+        ref = orc.e2m1_encode(x / s)
+        bad = np.nonzero(o2.cpu().numpy() != ref)[0]
+        assert bad.size == 0, (c, x[bad[:4]])
+    for b in list(range(1, 255, 17)) + [1, 127, 254]:
+        mp.convert(0x200 + b, xd_base, out)
+        torch.cuda.synchronize()
+        with np.errstate(over="ignore"):
+            ref = orc.e2m1_encode(np.ldexp(base, -(b - 127)).astype(np.float32))
+        bad = np.nonzero(out.cpu().numpy() != ref)[0]
+        assert bad.size == 0, (b, base[bad[:4]])
