@@ -24,8 +24,17 @@
  *    mpfa_prefill and mpfa_decode_paged, so both may be captured in a HIP
  *    graph.  mpfa_quantize_qk does not allocate either.
  *  - Data-dependent conditions (page index out of range, non-finite inputs,
- *    kv_len larger than the page table) are NOT checked on the device: the
- *    caller guarantees them.
+ *    kv_len larger than the page table) are NOT checked by the release
+ *    library (libmpfa.so): the caller guarantees them.  The debug library
+ *    (libmpfa_debug.so, same ABI) checks them before launching anything and
+ *    returns MPFA_ERR_DATA: it copies cu_seqlens, q_start, kv_len, the page
+ *    table rows in use and slot_mapping to the host, scans Q/K/V for
+ *    non-finite values on the device, and so synchronizes the stream and
+ *    allocates a 4-byte flag per call.  Checked: sequence lengths consistent
+ *    with cu_seqlens / total_tokens / max_seqlen; slots in [0, 64 num_pages);
+ *    q_start >= 0 and q_start + query tokens <= kv_len <= 64 max_pages; decode
+ *    kv_len >= 1 and within max_partitions partitions; page-table entries of
+ *    the pages in use >= 0, and < num_pages when the arguments carry it.
  *  - The library holds no mutable global state; concurrent calls on
  *    different streams are safe when their output buffers do not overlap.
  *
@@ -64,7 +73,9 @@ typedef enum {
     MPFA_ERR_INVALID = 1,      /* bad argument value or null pointer          */
     MPFA_ERR_UNSUPPORTED = 2,  /* valid request this build does not implement */
     MPFA_ERR_WORKSPACE = 3,    /* workspace missing or too small              */
-    MPFA_ERR_HIP = 4           /* a HIP launch or runtime call failed         */
+    MPFA_ERR_HIP = 4,          /* a HIP launch or runtime call failed         */
+    MPFA_ERR_DATA = 5          /* debug build only: the contents of an input
+                                  break a precondition (see below)            */
 } mpfa_status;
 
 #define MPFA_HEAD_DIM 128
@@ -206,7 +217,8 @@ typedef struct {
     void* out;                /* bf16 [T][h_q][128]                              */
     const void* v_aux;        /* with MPFA_PV_BF16 / MPFA_PV_NVFP4; else ignored */
     int64_t num_pages;        /* cache capacity in pages (plane offset of an NVFP4
-                                 v_aux); read only with MPFA_PV_NVFP4            */
+                                 v_aux); read with MPFA_PV_NVFP4 and by the debug
+                                 library's page index check (0 = not given)       */
 } mpfa_prefill_args;
 
 mpfa_status mpfa_prefill(const mpfa_prefill_args* args, mpfa_stream_t stream);
@@ -245,6 +257,8 @@ typedef struct {
     const void* ds;
     const float* k_tscale;    /* [batch][h_kv]                                    */
     void* out;                /* bf16 [batch][h_q][128]                           */
+    int64_t num_pages;        /* cache capacity in pages, 0 = not given; only the
+                                 debug library reads it (page index check)        */
 } mpfa_decode_args;
 
 /* Bytes of decode workspace: batch * h_q * max_partitions * (128 + 2) * 4. */

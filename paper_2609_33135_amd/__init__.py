@@ -10,9 +10,13 @@ import ctypes as C
 import os
 
 PKG_DIR = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG_DIR, "libmpfa.so")
+DEBUG_LIB_PATH = os.path.join(PKG_DIR, "libmpfa_debug.so")
+# MPFA_DEBUG=1 loads the twin library whose entry points also check the data
+# they are handed (index ranges, non-finite inputs) before launching
+LIB_PATH = DEBUG_LIB_PATH if os.environ.get("MPFA_DEBUG") == "1" else os.path.join(PKG_DIR, "libmpfa.so")
 
-MPFA_OK, MPFA_ERR_INVALID, MPFA_ERR_UNSUPPORTED, MPFA_ERR_WORKSPACE, MPFA_ERR_HIP = range(5)
+(MPFA_OK, MPFA_ERR_INVALID, MPFA_ERR_UNSUPPORTED, MPFA_ERR_WORKSPACE, MPFA_ERR_HIP,
+ MPFA_ERR_DATA) = range(6)
 SMOOTH, COMPUTE_STATS, TSCALE_UNIT, SEED_INIT, MXFP4, SEED_ELEMWISE = 1, 2, 4, 8, 16, 32
 PV_BF16, PV_NVFP4 = 64, 128
 HEAD_DIM, PAGE, TILE = 128, 64, 128
@@ -58,19 +62,29 @@ class DecodeArgs(C.Structure):
                 ("flags", C.c_uint32), ("kv_len", C.c_void_p), ("page_table", C.c_void_p),
                 ("q_codes", C.c_void_p), ("q_scales", C.c_void_p), ("q_tscale", C.c_void_p),
                 ("k_codes", C.c_void_p), ("k_scales", C.c_void_p), ("v_codes", C.c_void_p),
-                ("ds", C.c_void_p), ("k_tscale", C.c_void_p), ("out", C.c_void_p)]
+                ("ds", C.c_void_p), ("k_tscale", C.c_void_p), ("out", C.c_void_p),
+                ("num_pages", C.c_int64)]
 
 
-_lib = None
+_libs: dict = {}
 
 
 def lib():
     """Load libmpfa.so (built in-tree by build.py); raise if it is missing."""
-    global _lib
-    if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is not built; run paper_2609_33135_amd/build.py")
-        L = C.CDLL(LIB_PATH)
+    return _load(LIB_PATH)
+
+
+def debug_lib():
+    """Load libmpfa_debug.so: the same kernels behind entry points that also
+    check the data (index ranges, non-finite inputs) and return MPFA_ERR_DATA."""
+    return _load(DEBUG_LIB_PATH)
+
+
+def _load(path):
+    if path not in _libs:
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is not built; run paper_2609_33135_amd/build.py")
+        L = C.CDLL(path)
         L.mpfa_quantize_qk.restype = C.c_int
         L.mpfa_quantize_qk.argtypes = [C.POINTER(QuantArgs), C.c_void_p]
         L.mpfa_prefill.restype = C.c_int
@@ -94,8 +108,8 @@ def lib():
         L.mpfa_status_string.restype = C.c_char_p
         L.mpfa_status_string.argtypes = [C.c_int]
         L.mpfa_version.restype = C.c_char_p
-        _lib = L
-    return _lib
+        _libs[path] = L
+    return _libs[path]
 
 
 def status_string(s: int) -> str:
@@ -216,7 +230,7 @@ def decode_paged(qq: QuantQ, cache: PagedCache, stats: SeqStats, kv_len, page_ta
                    q_scales=_ptr(qq.scales), q_tscale=_ptr(qq.tscale),
                    k_codes=_ptr(cache.k_codes), k_scales=_ptr(cache.k_scales),
                    v_codes=_ptr(cache.v_codes), ds=_ptr(cache.ds),
-                   k_tscale=_ptr(stats.k_tscale), out=_ptr(out))
+                   k_tscale=_ptr(stats.k_tscale), out=_ptr(out), num_pages=cache.num_pages)
     _check(lib().mpfa_decode_paged(C.byref(a), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream)),
            "mpfa_decode_paged")
@@ -251,7 +265,7 @@ def mixed_step(pre: dict, dec: dict, workspace, flags: int, stream=None):
                     q_codes=_ptr(qd.codes), q_scales=_ptr(qd.scales), q_tscale=_ptr(qd.tscale),
                     k_codes=_ptr(dcache.k_codes), k_scales=_ptr(dcache.k_scales),
                     v_codes=_ptr(dcache.v_codes), ds=_ptr(dcache.ds), k_tscale=_ptr(dstats.k_tscale),
-                    out=_ptr(dec["out"]))
+                    out=_ptr(dec["out"]), num_pages=dcache.num_pages)
     _check(lib().mpfa_mixed_step(C.byref(pa), C.byref(da), _ptr(workspace),
                                  workspace.numel() * workspace.element_size(), _stream(stream)),
            "mpfa_mixed_step")

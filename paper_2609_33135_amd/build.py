@@ -1,4 +1,5 @@
-"""Build libmpfa.so (HIP kernels for gfx950 + the C ABI) in-tree with hipcc."""
+"""Build libmpfa.so (HIP kernels for gfx950 + the C ABI) and its data-checking
+twin libmpfa_debug.so in-tree with hipcc."""
 from __future__ import annotations
 
 import os
@@ -13,7 +14,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmpfa.so")
 
-SOURCES = ["api.cpp", "quantize.hip", "prefill.hip", "decode.hip", "mixed.hip"]
+SOURCES = ["api.cpp", "quantize.hip", "prefill.hip", "decode.hip", "mixed.hip", "debug_checks.hip"]
+DEBUG_LIB = os.path.join(PKG, "libmpfa_debug.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CLANG = os.environ.get("MPFA_CLANG", "/opt/rocm/lib/llvm/bin/clang++")
 ARCH = os.environ.get("MPFA_ARCH", "gfx950")
@@ -26,9 +28,10 @@ COMMON = [
 ]
 
 
-def _compile(src: str) -> str:
-    out = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [CLANG, "-x", "hip", *COMMON, "-c", os.path.join(CSRC, src), "-o", out]
+def _compile(src: str, debug: bool = False) -> str:
+    out = os.path.join(BUILD, os.path.splitext(src)[0] + ("_debug" if debug else "") + ".o")
+    extra = ["-DMPFA_DEBUG_CHECKS"] if debug else []
+    cmd = [CLANG, "-x", "hip", *COMMON, *extra, "-c", os.path.join(CSRC, src), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
     msg = "\n".join(l for l in (r.stdout + r.stderr).splitlines() if noise not in l)
@@ -39,18 +42,27 @@ def _compile(src: str) -> str:
     return out
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+def _link(out: str, objs: list[str]) -> None:
+    tmp = out + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source, then link libmpfa.so and libmpfa_debug.so (the same
+    kernels; its entry points also check the data they are handed)."""
+    os.makedirs(BUILD, exist_ok=True)
+    jobs = [(s, False) for s in SOURCES] + [("api.cpp", True)]
+    with ThreadPoolExecutor(max_workers=len(jobs)) as ex:
+        objs = list(ex.map(lambda j: _compile(*j), jobs))
+    kernels = objs[1:len(SOURCES)]
+    _link(LIB, [objs[0], *kernels])
+    _link(DEBUG_LIB, [objs[-1], *kernels])
     if verbose:
-        print("built", LIB)
+        print("built", LIB, DEBUG_LIB)
     return LIB
 
 

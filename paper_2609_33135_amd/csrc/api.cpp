@@ -10,6 +10,10 @@
 
 #include "mpfa_internal.h"
 
+#ifdef MPFA_DEBUG_CHECKS
+#include <vector>
+#endif
+
 namespace {
 
 constexpr int kPrefillRows = 256;   // query rows per prefill workgroup
@@ -23,6 +27,91 @@ bool heads_ok(int h_q, int h_kv) {
 
 // partition counters of the fused step follow the decode states, 256-byte aligned
 size_t mixed_counter_offset(size_t state_bytes) { return (state_bytes + 255) / 256 * 256; }
+
+#ifdef MPFA_DEBUG_CHECKS
+// ---- data checks of the debug library: index arrays copied to the host after
+// the stream's earlier work, inputs scanned for non-finite values on the device
+template <typename T>
+bool to_host(const T* dev, size_t n, std::vector<T>& out) {
+  out.resize(n);
+  return n == 0 || hipMemcpy(out.data(), dev, n * sizeof(T), hipMemcpyDeviceToHost) == hipSuccess;
+}
+
+mpfa_status scan_nonfinite(const void* x, int64_t n, hipStream_t s) {
+  int* flag = nullptr;
+  if (hipMalloc(&flag, sizeof(int)) != hipSuccess) return MPFA_ERR_HIP;
+  int h = 0;
+  const bool ok = hipMemsetAsync(flag, 0, sizeof(int), s) == hipSuccess &&
+                  mpfa::launch_scan_nonfinite(static_cast<const uint16_t*>(x), n, flag, s) == hipSuccess &&
+                  hipMemcpyAsync(&h, flag, sizeof(int), hipMemcpyDeviceToHost, s) == hipSuccess &&
+                  hipStreamSynchronize(s) == hipSuccess;
+  (void)hipFree(flag);
+  if (!ok) return MPFA_ERR_HIP;
+  return h ? MPFA_ERR_DATA : MPFA_OK;
+}
+
+// page-table entries of the pages a sequence of kv_len keys uses
+bool pages_ok(const std::vector<int32_t>& pt, int b, int max_pages, int kv_len, int64_t num_pages) {
+  for (int i = 0; i < (kv_len + 63) / 64; ++i) {
+    const int32_t e = pt[(size_t)b * max_pages + i];
+    if (e < 0 || (num_pages > 0 && e >= num_pages)) return false;
+  }
+  return true;
+}
+
+mpfa_status check_quant(const mpfa_quant_args* a, hipStream_t s) {
+  if (hipStreamSynchronize(s) != hipSuccess) return MPFA_ERR_HIP;
+  std::vector<int32_t> cu;
+  std::vector<int64_t> slots;
+  if (!to_host(a->cu_seqlens, (size_t)a->batch + 1, cu) || !to_host(a->slot_mapping, (size_t)a->total_tokens, slots))
+    return MPFA_ERR_HIP;
+  if (cu[0] != 0 || cu[a->batch] != a->total_tokens) return MPFA_ERR_DATA;
+  for (int b = 0; b < a->batch; ++b)
+    if (cu[b + 1] < cu[b] || cu[b + 1] - cu[b] > a->max_seqlen) return MPFA_ERR_DATA;
+  for (int64_t t = 0; t < a->total_tokens; ++t)
+    if (slots[t] < 0 || slots[t] >= 64 * a->num_pages) return MPFA_ERR_DATA;
+  if (a->flags & MPFA_PV_NVFP4)   // fresh prefill: token i at slot i % 64 of its page
+    for (int b = 0; b < a->batch; ++b)
+      for (int64_t i = 0; i < cu[b + 1] - cu[b]; ++i) {
+        const int64_t first = slots[cu[b] + i - i % 64];
+        if (first % 64 != 0 || slots[cu[b] + i] != first + i % 64) return MPFA_ERR_DATA;
+      }
+  const int64_t T = a->total_tokens;
+  mpfa_status st = scan_nonfinite(a->q, T * a->h_q * MPFA_HEAD_DIM, s);
+  if (st == MPFA_OK) st = scan_nonfinite(a->k, T * a->h_kv * MPFA_HEAD_DIM, s);
+  if (st == MPFA_OK) st = scan_nonfinite(a->v, T * a->h_kv * MPFA_HEAD_DIM, s);
+  return st;
+}
+
+mpfa_status check_prefill(const mpfa_prefill_args* a, hipStream_t s) {
+  if (hipStreamSynchronize(s) != hipSuccess) return MPFA_ERR_HIP;
+  std::vector<int32_t> cu, qs, kv, pt;
+  if (!to_host(a->cu_seqlens_q, (size_t)a->batch + 1, cu) || !to_host(a->q_start, (size_t)a->batch, qs) ||
+      !to_host(a->kv_len, (size_t)a->batch, kv) || !to_host(a->page_table, (size_t)a->batch * a->max_pages, pt))
+    return MPFA_ERR_HIP;
+  for (int b = 0; b < a->batch; ++b) {
+    const int n = cu[b + 1] - cu[b];
+    if (n < 0 || n > a->max_seqlen_q || qs[b] < 0 || (int64_t)qs[b] + n > kv[b] ||
+        (int64_t)kv[b] > 64LL * a->max_pages || !pages_ok(pt, b, a->max_pages, kv[b], a->num_pages))
+      return MPFA_ERR_DATA;
+  }
+  return MPFA_OK;
+}
+
+mpfa_status check_decode(const mpfa_decode_args* a, hipStream_t s) {
+  if (hipStreamSynchronize(s) != hipSuccess) return MPFA_ERR_HIP;
+  std::vector<int32_t> kv, pt;
+  if (!to_host(a->kv_len, (size_t)a->batch, kv) || !to_host(a->page_table, (size_t)a->batch * a->max_pages, pt))
+    return MPFA_ERR_HIP;
+  for (int b = 0; b < a->batch; ++b) {
+    if (kv[b] < 1 || (int64_t)kv[b] > 64LL * a->max_pages ||
+        (kv[b] + a->partition_tokens - 1) / a->partition_tokens > a->max_partitions ||
+        !pages_ok(pt, b, a->max_pages, kv[b], a->num_pages))
+      return MPFA_ERR_DATA;
+  }
+  return MPFA_OK;
+}
+#endif
 
 }  // namespace
 
@@ -137,6 +226,7 @@ const char* mpfa_status_string(mpfa_status s) {
     case MPFA_ERR_UNSUPPORTED: return "unsupported configuration";
     case MPFA_ERR_WORKSPACE: return "workspace missing or too small";
     case MPFA_ERR_HIP: return "HIP runtime error";
+    case MPFA_ERR_DATA: return "input data breaks a precondition (debug check)";
   }
   return "unknown status";
 }
@@ -193,14 +283,22 @@ mpfa_status mpfa_quantize_qk(const mpfa_quant_args* a, mpfa_stream_t stream) {
   p.pv = (a->flags & MPFA_PV_BF16) ? 1 : (a->flags & MPFA_PV_NVFP4) ? 2 : 0;
   p.v_aux = static_cast<uint8_t*>(a->v_aux);
   p.num_pages = a->num_pages;
+#ifdef MPFA_DEBUG_CHECKS
+  const mpfa_status dst = check_quant(a, reinterpret_cast<hipStream_t>(stream));
+  if (dst != MPFA_OK) return dst;
+#endif
   return mpfa::launch_quantize(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
                                                                                         : MPFA_ERR_HIP;
 }
 
 mpfa_status mpfa_prefill(const mpfa_prefill_args* a, mpfa_stream_t stream) {
   mpfa::PrefillParams p;
-  const mpfa_status st = prefill_params(a, p);
+  mpfa_status st = prefill_params(a, p);
   if (st != MPFA_OK) return st;
+#ifdef MPFA_DEBUG_CHECKS
+  st = check_prefill(a, reinterpret_cast<hipStream_t>(stream));
+  if (st != MPFA_OK) return st;
+#endif
   return mpfa::launch_prefill(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
                                                                                        : MPFA_ERR_HIP;
 }
@@ -233,8 +331,12 @@ mpfa_status mpfa_decode_choose_partition(int32_t batch, const int32_t* kv_len_ho
 mpfa_status mpfa_decode_paged(const mpfa_decode_args* a, void* workspace, size_t workspace_bytes,
                               mpfa_stream_t stream) {
   mpfa::DecodeParams p;
-  const mpfa_status st = decode_params(a, workspace, workspace_bytes, p);
+  mpfa_status st = decode_params(a, workspace, workspace_bytes, p);
   if (st != MPFA_OK) return st;
+#ifdef MPFA_DEBUG_CHECKS
+  st = check_decode(a, reinterpret_cast<hipStream_t>(stream));
+  if (st != MPFA_OK) return st;
+#endif
   return mpfa::launch_decode(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
                                                                                       : MPFA_ERR_HIP;
 }
@@ -281,6 +383,11 @@ mpfa_status mpfa_mixed_step(const mpfa_prefill_args* prefill, const mpfa_decode_
   m.stride = 1;
   m.first = 0;
   m.n_blocks = (int)(8 * (pre_rounds + n_rounds));
+#ifdef MPFA_DEBUG_CHECKS
+  st = check_prefill(prefill, reinterpret_cast<hipStream_t>(stream));
+  if (st == MPFA_OK) st = check_decode(decode, reinterpret_cast<hipStream_t>(stream));
+  if (st != MPFA_OK) return st;
+#endif
   return mpfa::launch_mixed(m, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
                                                                                     : MPFA_ERR_HIP;
 }

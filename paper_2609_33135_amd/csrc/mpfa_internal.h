@@ -94,6 +94,7 @@ struct MixedParams {
 };
 
 hipError_t launch_quantize(const QuantParams& p, hipStream_t stream);
+hipError_t launch_scan_nonfinite(const uint16_t* x, int64_t n, int* flag, hipStream_t stream);
 hipError_t launch_mixed(const MixedParams& m, hipStream_t stream);
 hipError_t launch_convert(int fmt, const float* x, int64_t n, uint8_t* out, hipStream_t stream);
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);

@@ -39,9 +39,21 @@ def test_exports_every_declared_symbol(mp):
     assert set(mp.EXPORTED) == names
 
 
+def test_debug_library_exports_the_same_symbols(mp):
+    names = _declared()
+    L = C.CDLL(mp.DEBUG_LIB_PATH)
+    for n in sorted(names):
+        assert hasattr(L, n), f"{n} missing from the debug library"
+    assert mp.debug_lib().mpfa_version().decode() == mp.lib().mpfa_version().decode()
+    # host validation is shared: bad arguments fail the same way without a GPU
+    a = _prefill_args(mp, h_q=7)
+    assert mp.debug_lib().mpfa_prefill(C.byref(a), None) == 1
+
+
 def test_status_strings(mp):
-    for s in range(5):
+    for s in range(6):
         assert mp.status_string(s)
+    assert "data" in mp.status_string(mp.MPFA_ERR_DATA)
     assert mp.lib().mpfa_version().decode().startswith("mpfa")
 
 
