@@ -185,7 +185,9 @@ __device__ __forceinline__ f32x4 mfma_fp4(u32x4 a, u32x4 b, f32x4 c, int scale_a
 
 // Four FP32 values in [0, 448] -> four E4M3 bytes (hardware RNE).
 __device__ __forceinline__ uint32_t pack_fp8x4(float a, float b, float c, float d) {
-  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  // both halves of the word are written, so its previous contents do not
+  // matter: passing a's bits lets the result take a's register
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, __float_as_int(a), false);
   w = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
   return (uint32_t)w;
 }

@@ -30,8 +30,17 @@ struct PrefillSmemT {
   // BF16 / NVFP4: [channel][key] BF16 or exact FP16, 256-byte rows of 16
   // chunks, chunk c of channel d stored at position c ^ (d & 15).
   uint8_t v[kD * kTile * (PV == kPvFp8 ? 1 : 2)];
-  uint16_t ds[kTile];       // BF16 seed values in accumulator units
+  float ds[kTile];          // seed values (BF16 values in accumulator units) as FP32, key order
+  // the same values ordered for the rank-one seed MFMA: the 8 values lane lr
+  // contributes (row lr of key blocks 0..7) are contiguous, one 16-byte read
+  uint16_t dss[kTile];
 };
+
+// position in PrefillSmemT::dss of key `key`: MFMA row 4*(key/32) + key%4 of
+// 16-key block (key/4)%8 (the key permutation of the score blocks)
+__device__ __forceinline__ int seed_slot(int key) {
+  return (4 * (key >> 5) + (key & 3)) * 8 + ((key >> 2) & 7);
+}
 
 // chunk swizzles: conflict-free 16-byte reads for the MFMA operand patterns
 __device__ __forceinline__ int k_swz(int key) { return (((key >> 5) << 2) | (key & 3)) & 15; }
@@ -168,7 +177,11 @@ __device__ __forceinline__ void store_tile(PrefillSmemT<PV>& sm, const TileRegs<
     }
   }
   // exact: a BF16 value times a power of two stays a BF16 value
-  if (t < kTile) sm.ds[t] = bf16_rne(bf16_to_f32((uint16_t)r.ds) * seed_scale);
+  if (t < kTile) {
+    const uint16_t v = bf16_rne(bf16_to_f32((uint16_t)r.ds) * seed_scale);
+    sm.ds[t] = bf16_to_f32(v);
+    sm.dss[seed_slot(t)] = v;
+  }
 }
 
 // How the compensation 1 Delta_S^T (Sec. 4.3 Eq. 11) enters the score
@@ -186,87 +199,350 @@ __device__ __forceinline__ void store_tile(PrefillSmemT<PV>& sm, const TileRegs<
 //             values up to the FP32 rounding order.
 enum SeedMode { kSeedNone = 0, kSeedMfma = 1, kSeedInit = 2, kSeedElem = 3 };
 
-// One prefill work item (query head, 256-row query tile) executed by a whole
-// workgroup of kThreads threads; `bid` is the item's position in the dispatch
-// order (largest tiles first) and smem two tile buffers in LDS.
-template <int SEED, bool MX, int PV>
-__device__ __forceinline__ void prefill_item(const PrefillParams& p, int bid, PrefillSmemT<PV>* smem) {
+// Per-item state of one wave: the work item, the query operands, the softmax
+// scale and the row positions.
+struct ItemState {
+  int b, h, hk, q0, nq, qs, kvl, j_hi;
+  int lane, wave, g, lr;
+  int wrow0, wpos_min, wpos_max;
+  bool wave_active;
+  float lam2, seed_scale;
+  int pos[kNB];
+  f16x8 qop[kNB][4];   // NVFP4: exact FP16 query operands, tensor scale factored out
+  u32x4 qraw[kNB];     // MXFP4: raw codes of channels 32g .. 32g+31
+  int qscale[kNB];     // MXFP4: their E8M0 scale
+  bf16x8 bseed;        // B operand of the rank-one seed MFMA: 1 in slot 0 of lanes 0..15
+};
 
-  // ---- work item: largest query tiles first (longest-processing-time order)
+// Decode work item `bid` (largest query tiles first, longest-processing-time
+// order) and load the wave's query operands.  Returns false when the item has
+// no rows.
+template <bool MX>
+__device__ __forceinline__ bool item_setup(const PrefillParams& p, int bid, ItemState& st) {
   int b, h, rank;
-  {
-    if (p.xcd_remap) {
-      // block ids are dealt round-robin to the 8 XCDs; give each XCD the query
-      // heads of a fixed subset of KV heads so their K/V tiles share its L2.
-      const int xcd = bid & 7, slot = bid >> 3;
-      const int kvpx = p.h_kv / 8, grp = p.h_q / p.h_kv;
-      const int ipr = kvpx * grp * p.batch;
-      rank = slot / ipr;
-      int r = slot % ipr;
-      const int hk = xcd * kvpx + r % kvpx;
-      r /= kvpx;
-      h = hk * grp + r % grp;
-      b = r / grp;
-    } else {
-      const int per = p.h_q * p.batch;
-      rank = bid / per;
-      const int rem = bid % per;
-      h = rem % p.h_q;
-      b = rem / p.h_q;
-    }
+  if (p.xcd_remap) {
+    // block ids are dealt round-robin to the 8 XCDs; give each XCD the query
+    // heads of a fixed subset of KV heads so their K/V tiles share its L2.
+    const int xcd = bid & 7, slot = bid >> 3;
+    const int kvpx = p.h_kv / 8, grp = p.h_q / p.h_kv;
+    const int ipr = kvpx * grp * p.batch;
+    rank = slot / ipr;
+    int r = slot % ipr;
+    const int hk = xcd * kvpx + r % kvpx;
+    r /= kvpx;
+    h = hk * grp + r % grp;
+    b = r / grp;
+  } else {
+    const int per = p.h_q * p.batch;
+    rank = bid / per;
+    const int rem = bid % per;
+    h = rem % p.h_q;
+    b = rem / p.h_q;
   }
   const int qtile = p.n_qtiles - 1 - rank;
   const int q0 = p.cu_seqlens_q[b];
   const int nq = p.cu_seqlens_q[b + 1] - q0;
   const int r0 = qtile * kQRows;
-  if (r0 >= nq) return;
+  if (r0 >= nq) return false;
 
-  const int qs = p.q_start[b], kvl = p.kv_len[b];
-  const int grp = p.h_q / p.h_kv, hk = h / grp;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 4, lr = lane & 15;
+  st.b = b;
+  st.h = h;
+  st.q0 = q0;
+  st.nq = nq;
+  st.qs = p.q_start[b];
+  st.kvl = p.kv_len[b];
+  st.hk = h / (p.h_q / p.h_kv);
+  st.lane = threadIdx.x & 63;
+  st.wave = threadIdx.x >> 6;
+  st.g = st.lane >> 4;
+  st.lr = st.lane & 15;
   const int last_row = min(r0 + kQRows, nq) - 1;
-  const int j_hi = (qs + last_row) >> 7;
+  st.j_hi = (st.qs + last_row) >> 7;
 
-  const float tq = p.q_tscale[b * p.h_q + h], tk = p.k_tscale[b * p.h_kv + hk];
+  const float tq = p.q_tscale[b * p.h_q + h], tk = p.k_tscale[b * p.h_kv + st.hk];
   const int eqk = ilog2f(tq) + ilog2f(tk);
-  const float lam2 = __builtin_ldexpf(p.lam, eqk);        // lambda * tQ * tK
-  const float seed_scale = __builtin_ldexpf(1.0f, -eqk);  // Delta_S in accumulator units
+  st.lam2 = __builtin_ldexpf(p.lam, eqk);        // lambda * tQ * tK
+  st.seed_scale = __builtin_ldexpf(1.0f, -eqk);  // Delta_S in accumulator units
 
-  const int wrow0 = r0 + wave * (kNB * 16);
-  const bool wave_active = wrow0 < nq;
-  const int wpos_min = qs + wrow0;
-  const int wpos_max = qs + min(wrow0 + kNB * 16, nq) - 1;
+  st.wrow0 = r0 + st.wave * (kNB * 16);
+  st.wave_active = st.wrow0 < nq;
+  st.wpos_min = st.qs + st.wrow0;
+  st.wpos_max = st.qs + min(st.wrow0 + kNB * 16, nq) - 1;
 
   // ---- Q operands (B of S^T = K Q^T).  NVFP4: exact FP16, tensor scale
   // factored out.  MXFP4: the raw codes of channels 32g .. 32g+31 and their
   // E8M0 scale (the lane's 32-element block of the scaled FP4 MFMA).
-  f16x8 qop[kNB][4];
-  u32x4 qraw[kNB];
-  int qscale[kNB];
-  int pos[kNB];
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
-    const int row = wrow0 + nb * 16 + lr;
-    pos[nb] = qs + row;
+    const int row = st.wrow0 + nb * 16 + st.lr;
+    st.pos[nb] = st.qs + row;
     const bool valid = row < nq;
     const int64_t tok = q0 + (valid ? row : 0);
     const uint8_t* qc = p.q_codes + (tok * p.h_q + h) * 64;
     const uint8_t* qsc = p.q_scales + (tok * p.h_q + h) * 8;
     if (MX) {
-      qraw[nb] = valid ? *reinterpret_cast<const u32x4*>(qc + 16 * g) : (u32x4){0u, 0u, 0u, 0u};
-      qscale[nb] = valid ? qsc[g] : 127;
+      st.qraw[nb] = valid ? *reinterpret_cast<const u32x4*>(qc + 16 * st.g) : (u32x4){0u, 0u, 0u, 0u};
+      st.qscale[nb] = valid ? qsc[st.g] : 127;
     } else {
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        const uint32_t cw = valid ? *reinterpret_cast<const uint32_t*>(qc + 16 * ks + 4 * g) : 0u;
-        const uint32_t sc = valid ? qsc[2 * ks + (g >> 1)] : 0u;
-        qop[nb][ks] = dequant8(cw, split_e4m3(sc));
+        const uint32_t cw = valid ? *reinterpret_cast<const uint32_t*>(qc + 16 * ks + 4 * st.g) : 0u;
+        const uint32_t sc = valid ? qsc[2 * ks + (st.g >> 1)] : 0u;
+        st.qop[nb][ks] = dequant8(cw, split_e4m3(sc));
       }
     }
   }
+  st.bseed = (bf16x8){};
+  if (st.lane < 16) st.bseed[0] = (__bf16)1.0f;
+  return true;
+}
 
-  bf16x8 bseed = {};
-  if (lane < 16) bseed[0] = (__bf16)1.0f;
+// S^T = seed + K Q^T of the tile in sm (Algorithm 1, scores of one tile).
+template <int SEED, bool MX, int PV>
+__device__ __forceinline__ void qk_tile(f32x4 (&s)[8][kNB], const PrefillSmemT<PV>& sm, const ItemState& st) {
+  const int g = st.g, lr = st.lr;
+  // rank-one seed operands: every lane reads the 8 values of its row lr;
+  // only reduction slot 0 of lanes 0..15 meets a nonzero B element, so the
+  // other (finite) values contribute exact zeros
+  const u32x4 dsv = SEED == kSeedMfma ? *reinterpret_cast<const u32x4*>(&sm.dss[8 * lr])
+                                      : (u32x4){0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int mb = 0; mb < 8; ++mb) {
+    f32x4 seed = (f32x4){0.f, 0.f, 0.f, 0.f};
+    if (SEED == kSeedMfma) {
+      const uint32_t w = dsv[mb >> 1];
+      const u32x4 a = {(mb & 1) ? (w >> 16) : w, 0u, 0u, 0u};
+      seed = mfma_bf16(__builtin_bit_cast(bf16x8, a), st.bseed, seed);
+    } else if (SEED == kSeedInit) {
+      // keys 32g + 4mb .. +3 of the lane's accumulator rows
+      seed = *reinterpret_cast<const f32x4*>(&sm.ds[32 * g + 4 * mb]);
+    }
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = seed;
+  }
+  if (MX) {
+    // one scaled FP4 MFMA per 16x16 block covers all 128 channels
+    const uint64_t ks8 = *reinterpret_cast<const uint64_t*>(sm.k + kMxScaleOff + (lr * 4 + g) * 8);
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+      const int krow = 32 * (lr >> 2) + 4 * mb + (lr & 3);
+      const u32x4 kop = *reinterpret_cast<const u32x4*>(sm.k + krow * 64 + ((g ^ mx_swz(krow)) << 4));
+      const int sk = (int)((ks8 >> (8 * mb)) & 0xFFu);
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_fp4(kop, st.qraw[nb], s[mb][nb], sk, st.qscale[nb]);
+    }
+  } else {
+#pragma unroll
+    for (int half = 0; half < 2; ++half)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+        for (int mb = 4 * half; mb < 4 * half + 4; ++mb) {
+          const int krow = 32 * (lr >> 2) + 4 * mb + (lr & 3);
+          const f16x8 kop = *reinterpret_cast<const f16x8*>(sm.k + krow * 256 + (((4 * ks + g) ^ lr) << 4));
+#pragma unroll
+          for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_f16(kop, st.qop[nb][ks], s[mb][nb]);
+        }
+      }
+  }
+  if (SEED == kSeedElem) {
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb)
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) s[mb][nb] += *reinterpret_cast<const f32x4*>(&sm.ds[32 * g + 4 * mb]);
+  }
+}
+
+// P operands of the PV product of one tile: FP8 words (kPvFp8) or eight
+// BF16 / exact FP16 values per MFMA (kPvBf16, kPvNvfp4).
+struct PTile {
+  i32x8 pb[kNB];
+  f16x8 ph[kNB][4];   // keys 32g + 8kk .. +7
+};
+
+// Causal mask, online softmax and P quantization of one tile (Algorithm 1,
+// softmax steps), with the rescale of O when a row maximum moved.
+template <int PV>
+__device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][kNB], int key0, bool need_mask, const ItemState& st,
+                                             float (&m)[kNB], float (&l)[kNB], f32x4 (&o)[8][kNB], PTile& pt) {
+  const int g = st.g;
+  const float lam2 = st.lam2;
+  if (need_mask) {
+    // key 32g + 4mb + i of the tile lies after query position pos
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb) {
+      const int lim = st.pos[nb] - key0 - 32 * g;
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (4 * mb + i > lim) s[mb][nb][i] = -INFINITY;
+        // keep each compare next to its select: scheduled as one batch, the
+        // 64 compare masks exhaust the scalar registers
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+  // log2 of the fixed factor the P quantizer applies: 448 (FP8), 1 (BF16),
+  // 2688 = 6 * 448 (NVFP4: the largest P, 1, maps to the top E2M1 code
+  // under the largest E4M3 scale)
+  constexpr float kLog2PScale = PV == kPvFp8 ? kLog2_448 : (PV == kPvBf16 ? 0.0f : 11.392317422778760f);
+  float alpha[kNB];
+#pragma unroll
+  for (int nb = 0; nb < kNB; ++nb) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb)
+      mx = fmaxf(fmaxf(mx, fmaxf(s[mb][nb][0], s[mb][nb][1])), fmaxf(s[mb][nb][2], s[mb][nb][3]));
+    mx = wave_max16(mx);
+    const float mnew = fmaxf(m[nb], mx);
+    const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
+    alpha[nb] = (m[nb] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m[nb] - muse) * lam2);
+    m[nb] = mnew;
+    const float bias = __builtin_fmaf(-muse, lam2, kLog2PScale);
+    float ps;
+    float ev[8][4];
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+      float e[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][nb][i], lam2, bias));
+      const float q4 = (e[0] + e[1]) + (e[2] + e[3]);
+      ps = mb == 0 ? q4 : ps + q4;
+      if (PV == kPvFp8) {
+        pt.pb[nb][mb] = (int)pack_fp8x4(e[0], e[1], e[2], e[3]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ev[mb][i] = e[i];
+      }
+    }
+    l[nb] = alpha[nb] * l[nb] + ps;
+    if (PV == kPvBf16) {
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        bf16x8 b;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          b[i] = (__bf16)ev[2 * kk][i];
+          b[4 + i] = (__bf16)ev[2 * kk + 1][i];
+        }
+        pt.ph[nb][kk] = __builtin_bit_cast(f16x8, b);
+      }
+    } else if (PV == kPvNvfp4) {
+      // the lane's 32 keys are two 16-key groups: keys 32g .. +15 (mb 0..3)
+      // and 32g + 16 .. +31 (mb 4..7); scale E4M3(amax / 6), codes E2M1(P'/scale)
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        float amax = 0.0f;
+#pragma unroll
+        for (int mb = 4 * half; mb < 4 * half + 4; ++mb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) amax = fmaxf(amax, ev[mb][i]);
+        const uint32_t sc = fp8_sat_pair(0u, div_by_scale(amax, 6.0f, kRcp6), 0.0f, false) & 0xFFu;
+        const float sd = e4m3_value(sc);
+        uint32_t cw[2] = {0u, 0u};
+        if (sd > 0.0f) {
+          const float r = __fdiv_rn(1.0f, sd);
+#pragma unroll
+          for (int w = 0; w < 2; ++w)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int mb = 4 * half + 2 * w + (j >> 1), i0 = 2 * (j & 1);
+              cw[w] = fp4_pair(cw[w], div_by_scale(ev[mb][i0], sd, r), div_by_scale(ev[mb][i0 + 1], sd, r),
+                               1.0f, j);
+            }
+        }
+        const ScaleSplit sp = split_e4m3(sc);
+        pt.ph[nb][2 * half] = dequant8(cw[0], sp);
+        pt.ph[nb][2 * half + 1] = dequant8(cw[1], sp);
+      }
+    }
+  }
+  bool moved = false;
+#pragma unroll
+  for (int nb = 0; nb < kNB; ++nb) moved |= alpha[nb] != 1.0f;
+  if (__builtin_amdgcn_ballot_w64(moved) != 0) {
+#pragma unroll
+    for (int db = 0; db < 8; ++db)
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) o[db][nb] *= alpha[nb];
+  }
+}
+
+// O^T += V^T P^T with V of the tile in sm.
+template <int PV>
+__device__ __forceinline__ void pv_tile(const PrefillSmemT<PV>& sm, const PTile& pt, f32x4 (&o)[8][kNB],
+                                        const ItemState& st) {
+  const int g = st.g, lr = st.lr;
+  if (PV == kPvFp8) {
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      const int d = 16 * db + lr;
+      const uint8_t* vr = sm.v + d * kTile;
+      const int sw = v_swz(d);
+      const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((2 * g) ^ sw) << 4));
+      const u32x4 vb = *reinterpret_cast<const u32x4*>(vr + (((2 * g + 1) ^ sw) << 4));
+      const i32x8 vop = {(int)va[0], (int)va[1], (int)va[2], (int)va[3],
+                         (int)vb[0], (int)vb[1], (int)vb[2], (int)vb[3]};
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) o[db][nb] = mfma_fp8(vop, pt.pb[nb], o[db][nb]);
+    }
+  } else {
+    // four 32-key MFMAs per channel block: MFMA kk reduces keys 32g + 8kk .. +7
+    // of every lane group g, so A (V row chunk 4g + kk) and B (the lane's own
+    // P values) pair the same keys
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      const uint8_t* vr = sm.v + (16 * db + lr) * (kTile * 2);
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((4 * g + kk) ^ lr) << 4));
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb) {
+          if (PV == kPvBf16)
+            o[db][nb] = mfma_bf16(__builtin_bit_cast(bf16x8, va), __builtin_bit_cast(bf16x8, pt.ph[nb][kk]),
+                                  o[db][nb]);
+          else
+            o[db][nb] = mfma_f16(__builtin_bit_cast(f16x8, va), pt.ph[nb][kk], o[db][nb]);
+        }
+      }
+    }
+  }
+}
+
+// out = O / (448 l) as BF16 (for the other PV precisions the factor is the
+// one their P carries).
+__device__ __forceinline__ void store_output(const PrefillParams& p, const ItemState& st, const float (&l)[kNB],
+                                             const f32x4 (&o)[8][kNB]) {
+#pragma unroll
+  for (int nb = 0; nb < kNB; ++nb) {
+    const float lt = wave_sum16(l[nb]);
+    const int row = st.wrow0 + nb * 16 + st.lr;
+    if (row < st.nq) {
+      uint16_t* dst = p.out + ((int64_t)(st.q0 + row) * p.h_q + st.h) * kD;
+      const float inv = __frcp_rn(lt);
+#pragma unroll
+      for (int db = 0; db < 8; ++db) {
+        const uint32_t lo = (uint32_t)bf16_rne(o[db][nb][0] * inv) |
+                            ((uint32_t)bf16_rne(o[db][nb][1] * inv) << 16);
+        const uint32_t hi = (uint32_t)bf16_rne(o[db][nb][2] * inv) |
+                            ((uint32_t)bf16_rne(o[db][nb][3] * inv) << 16);
+        *reinterpret_cast<uint2*>(dst + 16 * db + 4 * st.g) = make_uint2(lo, hi);
+      }
+    }
+  }
+}
+
+// One prefill work item (query head, 256-row query tile) executed by a whole
+// workgroup of kThreads threads; `bid` is the item's position in the dispatch
+// order (largest tiles first) and smem two tile buffers in LDS.  Every wave
+// runs QK, softmax and PV of a tile back to back; the next tile is fetched
+// into registers meanwhile and stored to the other buffer at the end.
+template <int SEED, bool MX, int PV>
+__device__ __forceinline__ void prefill_item(const PrefillParams& p, int bid, PrefillSmemT<PV>* smem) {
+  ItemState st;
+  if (!item_setup<MX>(p, bid, st)) return;
 
   float m[kNB], l[kNB];
   f32x4 o[8][kNB];
@@ -278,228 +554,31 @@ __device__ __forceinline__ void prefill_item(const PrefillParams& p, int bid, Pr
     for (int db = 0; db < 8; ++db) o[db][nb] = (f32x4){0.f, 0.f, 0.f, 0.f};
   }
 
-  const int32_t* pt = p.page_table + (int64_t)b * p.max_pages;
+  const int32_t* pt = p.page_table + (int64_t)st.b * p.max_pages;
   {
     TileRegs<PV> r0r;
-    fetch_tile<MX, PV>(r0r, p, pt, hk, h, j_hi, kvl);
-    store_tile<MX, PV>(smem[j_hi & 1], r0r, seed_scale);
+    fetch_tile<MX, PV>(r0r, p, pt, st.hk, st.h, st.j_hi, st.kvl);
+    store_tile<MX, PV>(smem[st.j_hi & 1], r0r, st.seed_scale);
   }
   __syncthreads();
-  for (int j = j_hi; j >= 0; --j) {
+  for (int j = st.j_hi; j >= 0; --j) {
     TileRegs<PV> nxt;
-    if (j > 0) fetch_tile<MX, PV>(nxt, p, pt, hk, h, j - 1, kvl);
+    if (j > 0) fetch_tile<MX, PV>(nxt, p, pt, st.hk, st.h, j - 1, st.kvl);
     const PrefillSmemT<PV>& sm = smem[j & 1];
     const int key0 = j * kTile;
-    if (wave_active && key0 <= wpos_max) {
-      const bool need_mask = key0 + kTile - 1 > wpos_min;
+    if (st.wave_active && key0 <= st.wpos_max) {
       f32x4 s[8][kNB];
-#pragma unroll
-      for (int mb = 0; mb < 8; ++mb) {
-        f32x4 seed = (f32x4){0.f, 0.f, 0.f, 0.f};
-        if (SEED == kSeedMfma) {
-          bf16x8 aseed = {};
-          aseed[0] = __builtin_bit_cast(__bf16, lane < 16 ? sm.ds[32 * (lr >> 2) + 4 * mb + (lr & 3)]
-                                                          : (uint16_t)0);
-          seed = mfma_bf16(aseed, bseed, seed);
-        } else if (SEED == kSeedInit) {
-          // keys 32g + 4mb .. +3 of the lane's accumulator rows
-          const uint2 d4 = *reinterpret_cast<const uint2*>(&sm.ds[32 * g + 4 * mb]);
-          seed = (f32x4){__uint_as_float(d4.x << 16), __uint_as_float(d4.x & 0xFFFF0000u),
-                         __uint_as_float(d4.y << 16), __uint_as_float(d4.y & 0xFFFF0000u)};
-        }
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = seed;
-      }
-      if (MX) {
-        // one scaled FP4 MFMA per 16x16 block covers all 128 channels
-        const uint64_t ks8 = *reinterpret_cast<const uint64_t*>(sm.k + kMxScaleOff + (lr * 4 + g) * 8);
-#pragma unroll
-        for (int mb = 0; mb < 8; ++mb) {
-          const int krow = 32 * (lr >> 2) + 4 * mb + (lr & 3);
-          const u32x4 kop = *reinterpret_cast<const u32x4*>(sm.k + krow * 64 + ((g ^ mx_swz(krow)) << 4));
-          const int sk = (int)((ks8 >> (8 * mb)) & 0xFFu);
-#pragma unroll
-          for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_fp4(kop, qraw[nb], s[mb][nb], sk, qscale[nb]);
-        }
-      } else {
-#pragma unroll
-        for (int half = 0; half < 2; ++half)
-#pragma unroll
-          for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-            for (int mb = 4 * half; mb < 4 * half + 4; ++mb) {
-              const int krow = 32 * (lr >> 2) + 4 * mb + (lr & 3);
-              const f16x8 kop = *reinterpret_cast<const f16x8*>(sm.k + krow * 256 + (((4 * ks + g) ^ lr) << 4));
-#pragma unroll
-              for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_f16(kop, qop[nb][ks], s[mb][nb]);
-            }
-          }
-      }
-      if (SEED == kSeedElem) {
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb)
-#pragma unroll
-          for (int mb = 0; mb < 8; ++mb) {
-            const uint2 d4 = *reinterpret_cast<const uint2*>(&sm.ds[32 * g + 4 * mb]);
-            s[mb][nb][0] += __uint_as_float(d4.x << 16);
-            s[mb][nb][1] += __uint_as_float(d4.x & 0xFFFF0000u);
-            s[mb][nb][2] += __uint_as_float(d4.y << 16);
-            s[mb][nb][3] += __uint_as_float(d4.y & 0xFFFF0000u);
-          }
-      }
-      if (need_mask) {
-#pragma unroll
-        for (int mb = 0; mb < 8; ++mb)
-#pragma unroll
-          for (int nb = 0; nb < kNB; ++nb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              if (key0 + 32 * g + 4 * mb + i > pos[nb]) s[mb][nb][i] = -INFINITY;
-      }
-      // log2 of the fixed factor the P quantizer applies: 448 (FP8), 1 (BF16),
-      // 2688 = 6 * 448 (NVFP4: the largest P, 1, maps to the top E2M1 code
-      // under the largest E4M3 scale)
-      constexpr float kLog2PScale = PV == kPvFp8 ? kLog2_448 : (PV == kPvBf16 ? 0.0f : 11.392317422778760f);
-      i32x8 pb[kNB];
-      f16x8 ph[kNB][4];   // BF16 (bit pattern) or dequantized NVFP4 P, keys 32g + 8kk .. +7
-      float alpha[kNB];
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int mb = 0; mb < 8; ++mb)
-          mx = fmaxf(fmaxf(mx, fmaxf(s[mb][nb][0], s[mb][nb][1])), fmaxf(s[mb][nb][2], s[mb][nb][3]));
-        mx = wave_max16(mx);
-        const float mnew = fmaxf(m[nb], mx);
-        const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
-        alpha[nb] = (m[nb] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m[nb] - muse) * lam2);
-        m[nb] = mnew;
-        const float bias = __builtin_fmaf(-muse, lam2, kLog2PScale);
-        float ps = 0.0f;
-        float ev[8][4];
-#pragma unroll
-        for (int mb = 0; mb < 8; ++mb) {
-          float e[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][nb][i], lam2, bias));
-          ps += (e[0] + e[1]) + (e[2] + e[3]);
-          if (PV == kPvFp8) {
-            pb[nb][mb] = (int)pack_fp8x4(e[0], e[1], e[2], e[3]);
-          } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) ev[mb][i] = e[i];
-          }
-        }
-        l[nb] = alpha[nb] * l[nb] + ps;
-        if (PV == kPvBf16) {
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk) {
-            bf16x8 b;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              b[i] = (__bf16)ev[2 * kk][i];
-              b[4 + i] = (__bf16)ev[2 * kk + 1][i];
-            }
-            ph[nb][kk] = __builtin_bit_cast(f16x8, b);
-          }
-        } else if (PV == kPvNvfp4) {
-          // the lane's 32 keys are two 16-key groups: keys 32g .. +15 (mb 0..3)
-          // and 32g + 16 .. +31 (mb 4..7); scale E4M3(amax / 6), codes E2M1(P'/scale)
-#pragma unroll
-          for (int half = 0; half < 2; ++half) {
-            float amax = 0.0f;
-#pragma unroll
-            for (int mb = 4 * half; mb < 4 * half + 4; ++mb)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) amax = fmaxf(amax, ev[mb][i]);
-            const uint32_t sc = fp8_sat_pair(0u, div_by_scale(amax, 6.0f, kRcp6), 0.0f, false) & 0xFFu;
-            const float sd = e4m3_value(sc);
-            uint32_t cw[2] = {0u, 0u};
-            if (sd > 0.0f) {
-              const float r = __fdiv_rn(1.0f, sd);
-#pragma unroll
-              for (int w = 0; w < 2; ++w)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                  const int mb = 4 * half + 2 * w + (j >> 1), i0 = 2 * (j & 1);
-                  cw[w] = fp4_pair(cw[w], div_by_scale(ev[mb][i0], sd, r), div_by_scale(ev[mb][i0 + 1], sd, r),
-                                   1.0f, j);
-                }
-            }
-            const ScaleSplit sp = split_e4m3(sc);
-            ph[nb][2 * half] = dequant8(cw[0], sp);
-            ph[nb][2 * half + 1] = dequant8(cw[1], sp);
-          }
-        }
-      }
-      bool moved = false;
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) moved |= alpha[nb] != 1.0f;
-      if (__builtin_amdgcn_ballot_w64(moved) != 0) {
-#pragma unroll
-        for (int db = 0; db < 8; ++db)
-#pragma unroll
-          for (int nb = 0; nb < kNB; ++nb) o[db][nb] *= alpha[nb];
-      }
-      if (PV == kPvFp8) {
-#pragma unroll
-        for (int db = 0; db < 8; ++db) {
-          const int d = 16 * db + lr;
-          const uint8_t* vr = sm.v + d * kTile;
-          const int sw = v_swz(d);
-          const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((2 * g) ^ sw) << 4));
-          const u32x4 vb = *reinterpret_cast<const u32x4*>(vr + (((2 * g + 1) ^ sw) << 4));
-          const i32x8 vop = {(int)va[0], (int)va[1], (int)va[2], (int)va[3],
-                             (int)vb[0], (int)vb[1], (int)vb[2], (int)vb[3]};
-#pragma unroll
-          for (int nb = 0; nb < kNB; ++nb) o[db][nb] = mfma_fp8(vop, pb[nb], o[db][nb]);
-        }
-      } else {
-        // four 32-key MFMAs per channel block: MFMA kk reduces keys 32g + 8kk .. +7
-        // of every lane group g, so A (V row chunk 4g + kk) and B (the lane's own
-        // P values) pair the same keys
-#pragma unroll
-        for (int db = 0; db < 8; ++db) {
-          const uint8_t* vr = sm.v + (16 * db + lr) * (kTile * 2);
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk) {
-            const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((4 * g + kk) ^ lr) << 4));
-#pragma unroll
-            for (int nb = 0; nb < kNB; ++nb) {
-              if (PV == kPvBf16)
-                o[db][nb] = mfma_bf16(__builtin_bit_cast(bf16x8, va), __builtin_bit_cast(bf16x8, ph[nb][kk]),
-                                      o[db][nb]);
-              else
-                o[db][nb] = mfma_f16(__builtin_bit_cast(f16x8, va), ph[nb][kk], o[db][nb]);
-            }
-          }
-        }
-      }
+      qk_tile<SEED, MX, PV>(s, sm, st);
+      PTile ptile;
+      softmax_tile<PV>(s, key0, key0 + kTile - 1 > st.wpos_min, st, m, l, o, ptile);
+      pv_tile<PV>(sm, ptile, o, st);
     }
-    if (j > 0) store_tile<MX, PV>(smem[(j - 1) & 1], nxt, seed_scale);
+    if (j > 0) store_tile<MX, PV>(smem[(j - 1) & 1], nxt, st.seed_scale);
     __syncthreads();
   }
 
-  if (!wave_active) return;
-  // ---- epilogue: out = O / (448 l), BF16
-#pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
-    const float lt = wave_sum16(l[nb]);
-    const int row = wrow0 + nb * 16 + lr;
-    if (row < nq) {
-      uint16_t* dst = p.out + ((int64_t)(q0 + row) * p.h_q + h) * kD;
-      const float inv = __frcp_rn(lt);
-#pragma unroll
-      for (int db = 0; db < 8; ++db) {
-        const uint32_t lo = (uint32_t)bf16_rne(o[db][nb][0] * inv) |
-                            ((uint32_t)bf16_rne(o[db][nb][1] * inv) << 16);
-        const uint32_t hi = (uint32_t)bf16_rne(o[db][nb][2] * inv) |
-                            ((uint32_t)bf16_rne(o[db][nb][3] * inv) << 16);
-        *reinterpret_cast<uint2*>(dst + 16 * db + 4 * g) = make_uint2(lo, hi);
-      }
-    }
-  }
+  if (!st.wave_active) return;
+  store_output(p, st, l, o);
 }
 
 }  // namespace
