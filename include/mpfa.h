@@ -84,25 +84,29 @@ typedef enum {
 #define MPFA_MAX_HEADS 256
 
 /* flags */
-#define MPFA_SMOOTH        1u  /* sequence centering + Delta_S compensation (off = "direct") */
+#define MPFA_SMOOTH        1u  /* sequence centering + Delta_S compensation (off = "direct");
+                                  prefill starts each QK accumulator at the rank-one term
+                                  1 Delta_S^T (Sec. 4.3 Eq. 11) loaded as the MFMA
+                                  accumulator input                                         */
 #define MPFA_COMPUTE_STATS 2u  /* compute means and K tensor scales from this call's tokens  */
 #define MPFA_TSCALE_UNIT   4u  /* NVFP4 tensor scale fixed to 1 (Eq. 1 without a 2nd level) */
-#define MPFA_SEED_INIT     8u  /* prefill: load the rank-one term 1 Delta_S^T as the input
-                                  accumulator of the first QK MFMA instead of issuing the
-                                  BF16 rank-one MFMA; results are bit-identical            */
+#define MPFA_SEED_MFMA     8u  /* prefill: form the rank-one term 1 Delta_S^T with one BF16
+                                  MFMA per 16-key block (Delta_S in reduction slot 0, ones
+                                  in B), the paper's formulation (Sec. 5.2), instead of
+                                  loading it as the accumulator input; bit-identical       */
 #define MPFA_SEED_ELEMWISE 32u /* prefill: the placement the rank-one seed replaces (Sec. 3.2,
                                   Sec. 7.4 Fig. 10), kept for comparison: the QK accumulator
                                   starts at zero and Delta_S is added to every score in FP32
                                   after the product, before masking.  Agrees with the seeded
                                   placements up to FP32 rounding order (not bit-identical).
-                                  Exclusive with MPFA_SEED_INIT.                          */
+                                  Exclusive with MPFA_SEED_MFMA.                          */
 #define MPFA_PV_BF16      64u  /* quantize + prefill: precision assignment NVFP4(QK) + BF16(PV)
                                   of the characterization in Sec. 3.1 / Fig. 3a: the
                                   quantizer also stores V in BF16 in v_aux (bf16
                                   [P][H_kv][128][64], channel-major like v_codes), and the
                                   prefill rounds P to BF16 (no scale) and runs PV on the
                                   BF16 MFMA over v_aux.  Not with MPFA_MXFP4,
-                                  MPFA_SEED_INIT or MPFA_SEED_ELEMWISE; decode: unsupported. */
+                                  MPFA_SEED_MFMA or MPFA_SEED_ELEMWISE; decode: unsupported. */
 #define MPFA_PV_NVFP4    128u  /* quantize + prefill: NVFP4(QK) + NVFP4(PV), the other arm of
                                   Fig. 3a: the quantizer stores V as NVFP4 in 16-key groups
                                   per channel in v_aux (a code plane u8 [P][H_kv][128][32],
@@ -200,7 +204,7 @@ typedef struct {
     int32_t batch, h_q, h_kv, head_dim;
     int32_t max_seqlen_q;     /* host: max query tokens of one sequence          */
     int32_t max_pages;        /* page_table row length                           */
-    uint32_t flags;           /* MPFA_SMOOTH, MPFA_SEED_INIT or MPFA_SEED_ELEMWISE, MPFA_MXFP4,
+    uint32_t flags;           /* MPFA_SMOOTH, MPFA_SEED_MFMA or MPFA_SEED_ELEMWISE, MPFA_MXFP4,
                                  MPFA_PV_BF16 or MPFA_PV_NVFP4                   */
     const int32_t* cu_seqlens_q; /* [batch+1] query tokens                       */
     const int32_t* q_start;   /* [batch] absolute position of query 0            */
@@ -286,7 +290,7 @@ mpfa_status mpfa_decode_paged(const mpfa_decode_args* args, void* workspace, siz
  * Results are bit-identical to mpfa_prefill followed by mpfa_decode_paged
  * with the same arguments.  Both parts must use the same MPFA_SMOOTH /
  * MPFA_MXFP4 setting (else MPFA_ERR_INVALID); the prefill flags may not
- * contain MPFA_SEED_INIT, MPFA_SEED_ELEMWISE or the PV characterization
+ * contain MPFA_SEED_MFMA, MPFA_SEED_ELEMWISE or the PV characterization
  * flags (MPFA_ERR_UNSUPPORTED).  Each part is validated as by its own entry
  * point.
  * workspace: caller-owned device memory of at least

@@ -17,7 +17,7 @@ LIB_PATH = DEBUG_LIB_PATH if os.environ.get("MPFA_DEBUG") == "1" else os.path.jo
 
 (MPFA_OK, MPFA_ERR_INVALID, MPFA_ERR_UNSUPPORTED, MPFA_ERR_WORKSPACE, MPFA_ERR_HIP,
  MPFA_ERR_DATA) = range(6)
-SMOOTH, COMPUTE_STATS, TSCALE_UNIT, SEED_INIT, MXFP4, SEED_ELEMWISE = 1, 2, 4, 8, 16, 32
+SMOOTH, COMPUTE_STATS, TSCALE_UNIT, SEED_MFMA, MXFP4, SEED_ELEMWISE = 1, 2, 4, 8, 16, 32
 PV_BF16, PV_NVFP4 = 64, 128
 HEAD_DIM, PAGE, TILE = 128, 64, 128
 

@@ -121,14 +121,14 @@ static mpfa_status prefill_params(const mpfa_prefill_args* a, mpfa::PrefillParam
   if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
   if (a->batch < 1 || a->max_seqlen_q < 0 || a->max_pages < 1) return MPFA_ERR_INVALID;
   if (!heads_ok(a->h_q, a->h_kv)) return MPFA_ERR_INVALID;
-  if (a->flags & ~(MPFA_SMOOTH | MPFA_SEED_INIT | MPFA_SEED_ELEMWISE | MPFA_MXFP4 | MPFA_PV_BF16 |
+  if (a->flags & ~(MPFA_SMOOTH | MPFA_SEED_MFMA | MPFA_SEED_ELEMWISE | MPFA_MXFP4 | MPFA_PV_BF16 |
                    MPFA_PV_NVFP4))
     return MPFA_ERR_INVALID;
-  if ((a->flags & MPFA_SEED_INIT) && (a->flags & MPFA_SEED_ELEMWISE)) return MPFA_ERR_INVALID;
+  if ((a->flags & MPFA_SEED_MFMA) && (a->flags & MPFA_SEED_ELEMWISE)) return MPFA_ERR_INVALID;
   const uint32_t pvp = a->flags & (MPFA_PV_BF16 | MPFA_PV_NVFP4);
   if (pvp == (MPFA_PV_BF16 | MPFA_PV_NVFP4) || (pvp && !a->v_aux)) return MPFA_ERR_INVALID;
   if ((pvp & MPFA_PV_NVFP4) && a->num_pages < 1) return MPFA_ERR_INVALID;
-  if (pvp && (a->flags & (MPFA_MXFP4 | MPFA_SEED_INIT | MPFA_SEED_ELEMWISE))) return MPFA_ERR_UNSUPPORTED;
+  if (pvp && (a->flags & (MPFA_MXFP4 | MPFA_SEED_MFMA | MPFA_SEED_ELEMWISE))) return MPFA_ERR_UNSUPPORTED;
   const bool smooth = a->flags & MPFA_SMOOTH;
   if (!a->cu_seqlens_q || !a->q_start || !a->kv_len || !a->page_table || !a->q_codes ||
       !a->q_scales || !a->q_tscale || !a->k_codes || !a->k_scales || !a->v_codes ||
@@ -144,7 +144,7 @@ static mpfa_status prefill_params(const mpfa_prefill_args* a, mpfa::PrefillParam
   p.max_pages = a->max_pages;
   p.n_qtiles = (int)n_qtiles;
   p.smooth = smooth;
-  p.seed_init = (a->flags & MPFA_SEED_INIT) != 0;
+  p.seed_mfma = (a->flags & MPFA_SEED_MFMA) != 0;
   p.seed_elem = (a->flags & MPFA_SEED_ELEMWISE) != 0;
   p.pv = (a->flags & MPFA_PV_BF16) ? 1 : (a->flags & MPFA_PV_NVFP4) ? 2 : 0;
   p.v_aux = static_cast<const uint8_t*>(a->v_aux);
@@ -355,7 +355,7 @@ mpfa_status mpfa_mixed_step(const mpfa_prefill_args* prefill, const mpfa_decode_
   if (!prefill || !decode) return MPFA_ERR_INVALID;
   // the fused kernel runs the method's placements only (rank-one seed or none,
   // FP8 PV), with one smoothing / format setting for both parts
-  if (prefill->flags & (MPFA_SEED_INIT | MPFA_SEED_ELEMWISE | MPFA_PV_BF16 | MPFA_PV_NVFP4))
+  if (prefill->flags & (MPFA_SEED_MFMA | MPFA_SEED_ELEMWISE | MPFA_PV_BF16 | MPFA_PV_NVFP4))
     return MPFA_ERR_UNSUPPORTED;
   if ((prefill->flags & (MPFA_SMOOTH | MPFA_MXFP4)) != (decode->flags & (MPFA_SMOOTH | MPFA_MXFP4)))
     return MPFA_ERR_INVALID;

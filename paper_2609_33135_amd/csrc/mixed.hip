@@ -44,7 +44,7 @@ __global__ __launch_bounds__(512, 1) void mixed_kernel(MixedParams m) {
   if (!is_dec) {
     const int bid = i - 8 * dec_before;
     if (bid >= m.n_pre_blocks) return;
-    prefill_item<SMOOTH ? kSeedMfma : kSeedNone, MX, kPvFp8>(m.pre, bid,
+    prefill_item<SMOOTH ? kSeedInit : kSeedNone, MX, kPvFp8>(m.pre, bid,
                                                              reinterpret_cast<PrefillSmemT<kPvFp8>*>(lds));
     return;
   }

@@ -38,7 +38,7 @@ struct PrefillParams {
   int batch, h_q, h_kv, max_pages;
   int n_qtiles;     // max query tiles of one sequence
   int smooth;
-  int seed_init;    // 1: compensation loaded as the accumulator input, 0: rank-one MFMA
+  int seed_mfma;    // 1: compensation formed by the rank-one BF16 MFMA, 0: accumulator input
   int seed_elem;    // 1: compensation added to each score after the QK product
   int mx;           // Q/K in MXFP4: QK on the scaled FP4 MFMA
   int xcd_remap;    // 1: spread KV heads over the 8 XCDs (needs h_kv % 8 == 0)

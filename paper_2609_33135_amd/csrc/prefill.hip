@@ -6,9 +6,10 @@
 //   * the workgroup stages the tile in LDS: NVFP4 K dequantized once to exact
 //     FP16 (group scale applied, tensor scale factored out), FP8 V in its
 //     channel-major page layout, and the compensation vector Delta_S;
-//   * each wave computes S^T = K Q^T on FP16 MFMA (16x16x32), seeded by one
-//     BF16 rank-one MFMA per 16x16 block that writes Delta_S into the
-//     accumulator first (Sec. 4.3 Eq. 11, Sec. 5.2);
+//   * each wave computes S^T = K Q^T on FP16 MFMA (16x16x32) starting from
+//     the rank-one term 1 Delta_S^T (Sec. 4.3 Eq. 11): loaded from LDS as the
+//     accumulator input, or (MPFA_SEED_MFMA) formed by one BF16 rank-one MFMA
+//     per 16x16 block as in Sec. 5.2;
 //   * mask, row max, P = 2^(lambda (S - m) + log2 448), row sum of the FP32 P,
 //     FP8 conversion in registers; the S^T accumulator layout is already the
 //     B-operand layout of the FP8 PV MFMA (O^T = V^T P^T), so P never leaves
@@ -38,20 +39,20 @@ hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream) {
   const dim3 grid(blocks), block(kThreads);
   if (p.pv == kPvBf16) {
     if (!p.smooth) prefill_kernel<kSeedNone, false, kPvBf16><<<grid, block, 0, stream>>>(p);
-    else prefill_kernel<kSeedMfma, false, kPvBf16><<<grid, block, 0, stream>>>(p);
+    else prefill_kernel<kSeedInit, false, kPvBf16><<<grid, block, 0, stream>>>(p);
   } else if (p.pv == kPvNvfp4) {
     if (!p.smooth) prefill_kernel<kSeedNone, false, kPvNvfp4><<<grid, block, 0, stream>>>(p);
-    else prefill_kernel<kSeedMfma, false, kPvNvfp4><<<grid, block, 0, stream>>>(p);
+    else prefill_kernel<kSeedInit, false, kPvNvfp4><<<grid, block, 0, stream>>>(p);
   } else if (p.mx) {
     if (!p.smooth) prefill_kernel<kSeedNone, true, kPvFp8><<<grid, block, 0, stream>>>(p);
-    else if (p.seed_init) prefill_kernel<kSeedInit, true, kPvFp8><<<grid, block, 0, stream>>>(p);
+    else if (p.seed_mfma) prefill_kernel<kSeedMfma, true, kPvFp8><<<grid, block, 0, stream>>>(p);
     else if (p.seed_elem) prefill_kernel<kSeedElem, true, kPvFp8><<<grid, block, 0, stream>>>(p);
-    else prefill_kernel<kSeedMfma, true, kPvFp8><<<grid, block, 0, stream>>>(p);
+    else prefill_kernel<kSeedInit, true, kPvFp8><<<grid, block, 0, stream>>>(p);
   } else {
     if (!p.smooth) prefill_kernel<kSeedNone, false, kPvFp8><<<grid, block, 0, stream>>>(p);
-    else if (p.seed_init) prefill_kernel<kSeedInit, false, kPvFp8><<<grid, block, 0, stream>>>(p);
+    else if (p.seed_mfma) prefill_kernel<kSeedMfma, false, kPvFp8><<<grid, block, 0, stream>>>(p);
     else if (p.seed_elem) prefill_kernel<kSeedElem, false, kPvFp8><<<grid, block, 0, stream>>>(p);
-    else prefill_kernel<kSeedMfma, false, kPvFp8><<<grid, block, 0, stream>>>(p);
+    else prefill_kernel<kSeedInit, false, kPvFp8><<<grid, block, 0, stream>>>(p);
   }
   return hipGetLastError();
 }

@@ -459,14 +459,13 @@ __device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][kNB], int key0, bool 
       }
     }
   }
-  bool moved = false;
+  // rescale the O rows of a query block only when one of its maxima moved
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) moved |= alpha[nb] != 1.0f;
-  if (__builtin_amdgcn_ballot_w64(moved) != 0) {
+  for (int nb = 0; nb < kNB; ++nb) {
+    if (__builtin_amdgcn_ballot_w64(alpha[nb] != 1.0f) != 0) {
 #pragma unroll
-    for (int db = 0; db < 8; ++db)
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) o[db][nb] *= alpha[nb];
+      for (int db = 0; db < 8; ++db) o[db][nb] *= alpha[nb];
+    }
   }
 }
 

@@ -110,7 +110,7 @@ def test_prefill_seed_modes_bit_identical(orc, mp):
     print("case: seed modes", flush=True)
     run = H.Run(orc, mp, 29, [700, 45], 8, 2)
     a = run.prefill_gpu()
-    b = run.prefill_gpu(extra_flags=mp.SEED_INIT)
+    b = run.prefill_gpu(extra_flags=mp.SEED_MFMA)
     assert np.array_equal(a, b)
 
 
@@ -139,13 +139,13 @@ def test_prefill_repeatable_all_modes(orc, mp):
     run = H.Run(orc, mp, 17, [1, 130, 300, 513], 8, 2, outliers=True, smooth=True)
     first = {}
     for _ in range(12):
-        for fl in (0, mp.SEED_INIT):
+        for fl in (0, mp.SEED_MFMA):
             out = run.prefill_gpu(extra_flags=fl)
             if fl in first:
                 assert np.array_equal(out, first[fl]), f"flags {fl}: output changed between launches"
             else:
                 first[fl] = out
-    assert np.array_equal(first[0], first[mp.SEED_INIT])
+    assert np.array_equal(first[0], first[mp.SEED_MFMA])
     direct = H.Run(orc, mp, 17, [1, 130, 300, 513], 8, 2, outliers=True, smooth=False)
     a = direct.prefill_gpu()
     for _ in range(6):
@@ -161,7 +161,7 @@ def test_prefill_mxfp4_ragged(orc, mp, smooth):
     out = run.prefill_gpu()
     _check(run, out, _all_items(seqlens, 8), label=f"mxfp4 smooth={smooth}")
     if smooth:
-        assert np.array_equal(out, run.prefill_gpu(extra_flags=mp.SEED_INIT))
+        assert np.array_equal(out, run.prefill_gpu(extra_flags=mp.SEED_MFMA))
     for _ in range(4):
         assert np.array_equal(run.prefill_gpu(), out)
 
