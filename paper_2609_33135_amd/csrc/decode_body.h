@@ -233,11 +233,16 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
           if (key0 + 32 * g + 4 * mb + i >= kend) s[mb][i] = -INFINITY;
     }
     // ---- online softmax (rows = query heads), P to FP8 (x448)
-    float mx = -INFINITY;
+    // two independent chains of v_max3 (two new scores per instruction)
+    float mxa = -INFINITY, mxb = -INFINITY;
 #pragma unroll
-    for (int mb = 0; mb < 8; ++mb)
-      mx = fmaxf(fmaxf(mx, fmaxf(s[mb][0], s[mb][1])), fmaxf(s[mb][2], s[mb][3]));
-    mx = wave_max16(mx);
+    for (int mb = 0; mb < 8; mb += 2) {
+      mxa = fmaxf(fmaxf(mxa, s[mb][0]), s[mb][1]);
+      mxa = fmaxf(fmaxf(mxa, s[mb][2]), s[mb][3]);
+      mxb = fmaxf(fmaxf(mxb, s[mb + 1][0]), s[mb + 1][1]);
+      mxb = fmaxf(fmaxf(mxb, s[mb + 1][2]), s[mb + 1][3]);
+    }
+    const float mx = wave_max16(fmaxf(mxa, mxb));
     const float mnew = fmaxf(m, mx);
     const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
     const float alpha = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m - muse) * lam2);

@@ -192,11 +192,19 @@ __device__ __forceinline__ uint32_t pack_fp8x4(float a, float b, float c, float 
   return (uint32_t)w;
 }
 
+// Maximum over the four lanes l, l^16, l^32, l^48 (the four 16-lane rows).
+// v_permlane16_swap exchanges the odd rows of its first operand with the even
+// rows of its second; with both operands x the two results hold, in every
+// lane, the values of rows {2r, 2r+1}.  v_permlane32_swap does the same for
+// the two halves of the wave.  Both are plain vector instructions (no LDS
+// round trip as a shuffle through ds_bpermute would take).
 __device__ __forceinline__ float wave_max16(float x) {
-  x = fmaxf(x, __shfl_xor(x, 16));
-  x = fmaxf(x, __shfl_xor(x, 32));
-  return x;
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
+
 __device__ __forceinline__ float wave_sum16(float x) {
   x += __shfl_xor(x, 16);
   x += __shfl_xor(x, 32);

@@ -390,11 +390,16 @@ __device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][kNB], int key0, bool 
   float alpha[kNB];
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
-    float mx = -INFINITY;
+    // two independent chains of v_max3 (two new scores per instruction)
+    float mxa = -INFINITY, mxb = -INFINITY;
 #pragma unroll
-    for (int mb = 0; mb < 8; ++mb)
-      mx = fmaxf(fmaxf(mx, fmaxf(s[mb][nb][0], s[mb][nb][1])), fmaxf(s[mb][nb][2], s[mb][nb][3]));
-    mx = wave_max16(mx);
+    for (int mb = 0; mb < 8; mb += 2) {
+      mxa = fmaxf(fmaxf(mxa, s[mb][nb][0]), s[mb][nb][1]);
+      mxa = fmaxf(fmaxf(mxa, s[mb][nb][2]), s[mb][nb][3]);
+      mxb = fmaxf(fmaxf(mxb, s[mb + 1][nb][0]), s[mb + 1][nb][1]);
+      mxb = fmaxf(fmaxf(mxb, s[mb + 1][nb][2]), s[mb + 1][nb][3]);
+    }
+    const float mx = wave_max16(fmaxf(mxa, mxb));
     const float mnew = fmaxf(m[nb], mx);
     const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
     alpha[nb] = (m[nb] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m[nb] - muse) * lam2);
