@@ -158,13 +158,35 @@ __global__ __launch_bounds__(256) void stats_partial_kernel(QuantParams p) {
   }
 }
 
-// One workgroup of 128 threads (one per channel) per (head, sequence): block
-// partials added in block order, FP32 divide, BF16 rounding; tensor scale from
-// the per-channel max / min.  Also covers sequences with no tokens and the
-// calls that need no per-token statistics at all (need_partials == 0).
-__global__ __launch_bounds__(128) void stats_final_kernel(QuantParams p) {
+// One workgroup of 512 threads per (head, sequence): block partials added in
+// block order, FP32 divide, BF16 rounding; tensor scale from the per-channel
+// max / min.  Also covers sequences with no tokens and the calls that need no
+// per-token statistics at all (need_partials == 0).  The partials arrive in
+// LDS 64 blocks at a time, loaded by all threads (coalesced 512-byte rows, the
+// next chunk in flight while the current one is added); threads 0..127 own one
+// channel each and add its partials strictly in block order.
+constexpr int kFinThreads = 512;
+constexpr int kFinChunk = 64;                                      // blocks per chunk
+constexpr int kFinLoads = 3 * kFinChunk * (kD / 4) / kFinThreads;  // float4 loads per thread and chunk
+
+__device__ __forceinline__ void fin_load(const QuantParams& p, int64_t t0, int nblk, int hs, int hh, int blk0,
+                                         float4 (&r)[kFinLoads]) {
+#pragma unroll
+  for (int i = 0; i < kFinLoads; ++i) {
+    const int idx = i * kFinThreads + (int)threadIdx.x;
+    const int arr = idx / (kFinChunk * (kD / 4)), rem = idx % (kFinChunk * (kD / 4));
+    const int blk = blk0 + rem / (kD / 4), q4 = rem % (kD / 4);
+    r[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (blk < nblk)
+      r[i] = *reinterpret_cast<const float4*>(partial_ptr(p, t0, nblk, blk, hs) + (int64_t)arr * hs * kD + hh * kD +
+                                              4 * q4);
+  }
+}
+
+__global__ __launch_bounds__(kFinThreads) void stats_final_kernel(QuantParams p) {
+  __shared__ float4 chunk[3 * kFinChunk * (kD / 4)];   // [sum, max, min][block][channel / 4]: 96 KB
   __shared__ float red[2];
-  const int hh = blockIdx.x, b = blockIdx.y, c = threadIdx.x;
+  const int hh = blockIdx.x, b = blockIdx.y, t = threadIdx.x, c = t;
   const int64_t t0 = p.cu_seqlens[b];
   const int n = p.cu_seqlens[b + 1] - (int)t0;
   const int nblk = (n + 127) >> 7;
@@ -173,39 +195,37 @@ __global__ __launch_bounds__(128) void stats_final_kernel(QuantParams p) {
   float tot = 0.0f, mx = -INFINITY, mn = INFINITY;
   const bool have = p.need_partials && nblk >= 2;
   if (have) {
-    // partials of 32 blocks in flight, added in block order
-    constexpr int kAhead = 32;
-    for (int blk0 = 0; blk0 < nblk; blk0 += kAhead) {
-      float ps[kAhead], px[kAhead], pn[kAhead];
+    float4 r[kFinLoads];
+    fin_load(p, t0, nblk, ss.hs, hh, 0, r);
+    for (int blk0 = 0; blk0 < nblk; blk0 += kFinChunk) {
 #pragma unroll
-      for (int j = 0; j < kAhead; ++j) {
-        ps[j] = 0.0f;
-        px[j] = -INFINITY;
-        pn[j] = INFINITY;
-        if (blk0 + j < nblk) {
-          const float* part = partial_ptr(p, t0, nblk, blk0 + j, ss.hs) + hh * kD + c;
-          ps[j] = part[0];
-          px[j] = part[ss.hs * kD];
-          pn[j] = part[2 * ss.hs * kD];
+      for (int i = 0; i < kFinLoads; ++i) chunk[i * kFinThreads + t] = r[i];
+      __syncthreads();
+      if (blk0 + kFinChunk < nblk) fin_load(p, t0, nblk, ss.hs, hh, blk0 + kFinChunk, r);
+      if (c < kD) {
+        const float* cs = reinterpret_cast<const float*>(chunk);
+        const int nb = min(kFinChunk, nblk - blk0);
+        for (int j = 0; j < nb; ++j) {
+          tot += cs[j * kD + c];
+          mx = fmaxf(mx, cs[(kFinChunk + j) * kD + c]);
+          mn = fminf(mn, cs[(2 * kFinChunk + j) * kD + c]);
         }
       }
-#pragma unroll
-      for (int j = 0; j < kAhead; ++j) {
-        if (blk0 + j < nblk) tot += ps[j];
-        mx = fmaxf(mx, px[j]);
-        mn = fminf(mn, pn[j]);
-      }
+      __syncthreads();
     }
   }
-  uint16_t* mrow = mean_row(p, b, hh);
-  uint16_t m = 0;
-  if (ss.want_sum && n > 0) m = bf16_rne(__fdiv_rn(tot, (float)n));
-  else if (!p.compute_stats && p.smooth) m = mrow[c];
-  if (p.compute_stats) mrow[c] = m;
-  const float mu = bf16_to_f32(m);
-  float amax = have ? fmaxf(__builtin_fabsf(mx - mu), __builtin_fabsf(mn - mu)) : 0.0f;
-  for (int off = 32; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
-  if ((c & 63) == 0) red[c >> 6] = amax;
+  float amax = 0.0f;
+  if (c < kD) {
+    uint16_t* mrow = mean_row(p, b, hh);
+    uint16_t m = 0;
+    if (ss.want_sum && n > 0) m = bf16_rne(__fdiv_rn(tot, (float)n));
+    else if (!p.compute_stats && p.smooth) m = mrow[c];
+    if (p.compute_stats) mrow[c] = m;
+    const float mu = bf16_to_f32(m);
+    amax = have ? fmaxf(__builtin_fabsf(mx - mu), __builtin_fabsf(mn - mu)) : 0.0f;
+    for (int off = 32; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
+    if ((c & 63) == 0) red[c >> 6] = amax;
+  }
   __syncthreads();
   if (c == 0) write_tscale(p, b, hh, fmaxf(red[0], red[1]));
 }
@@ -550,7 +570,7 @@ hipError_t launch_quantize(const QuantParams& p, hipStream_t stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  stats_final_kernel<<<dim3(hs, p.batch), dim3(128), 0, stream>>>(p);
+  stats_final_kernel<<<dim3(hs, p.batch), dim3(kFinThreads), 0, stream>>>(p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (p.total_tokens > 0 && p.max_seqlen > 0) {
