@@ -66,6 +66,17 @@ def test_quantize_modes(orc, mp, smooth, tunit):
     _assert_quant_equal(run, smooth=smooth)
 
 
+def test_quantize_statistics_chunk_boundaries(orc, mp):
+    """Sequences whose 128-token block counts straddle the 64-block chunks in
+    which the statistics finish stages the block partials: 65 blocks (one past
+    a chunk, the last block alone in its chunk), 64 (exactly one chunk), 129 (three
+    chunks) and 2; means, tensor scales and every code bit-exact."""
+    seqlens = [64 * 128 + 1, 64 * 128, 128 * 128 + 37, 129]
+    print(f"case: statistics chunk boundaries {seqlens} 4q/2kv seed 23", flush=True)
+    run = H.Run(orc, mp, 23, seqlens, 4, 2, outliers=True)
+    _assert_quant_equal(run)
+
+
 def test_quantize_llama_prefill_shape(orc, mp):
     """Full Llama-3.1-8B-shaped prefill workload (16384 tokens, 32q/8kv)."""
     print("case: llama prefill 16384 tokens 32q/8kv seed 2", flush=True)
