@@ -88,6 +88,8 @@ def parse():
     ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant runs")
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed serving step (separate launches vs one fused launch)")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the Llama-shaped prefill length sweep (16K, 32K, 64K tokens)")
     ap.add_argument("--no-precision", action="store_true",
                     help="skip the BF16 / NVFP4 PV precision-assignment runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -119,8 +121,8 @@ class Timer:
         return self.s.elapsed_time(self.e)
 
 
-def setup_prefill(torch, np, mp, W, seq, smooth, mx=False, pv=0):
-    wl = W.qwen_prefill(seq)
+def setup_prefill(torch, np, mp, W, seq, smooth, mx=False, pv=0, wl=None):
+    wl = wl if wl is not None else W.qwen_prefill(seq)
     dev = "cuda"
     q, k, v = W.gen_qkv(wl.seed, [seq], wl.h_q, wl.h_kv, wl.outliers, dev)
     pt, n_pages = W.make_pages(wl.seed, [seq])
@@ -500,6 +502,34 @@ def main():
                                     "quant_ms": mq_ms, "layer_ms": mq_ms + mx_ms}
             del sm
             torch.cuda.empty_cache()
+
+    if not args.no_prefill and not args.no_sweep:
+        # Llama-3.1-8B-shaped prefill over the paper's range of lengths (Sec. 7.2
+        # reports 16K-128K on this shape): NVFP4 (headline format) and MXFP4
+        sweep = {}
+        for n in (16384, 32768, 65536):
+            wl_n = W.llama_prefill(n)
+            f_n = 4.0 * 128 * wl_n.causal_pairs()
+            row = {}
+            for name, mx in (("nvfp4", False), ("mxfp4", True)):
+                log(f"prefill sweep: llama shape {n} tokens, {name} ...")
+                sw = setup_prefill(torch, np, mp, W, n, smooth=True, mx=mx, wl=wl_n)
+                run_quant(mp, sw)
+                for _ in range(max(args.warmup, 1)):
+                    run_prefill(mp, sw)
+                torch.cuda.synchronize()
+                ts = []
+                for _ in range(args.steps):
+                    with Timer(torch) as t2:
+                        run_prefill(mp, sw)
+                    ts.append(t2)
+                torch.cuda.synchronize()
+                ms = sum(t.ms() for t in ts) / args.steps
+                row[name] = {"ms": ms, "tflops": f_n / (ms * 1e-3) / 1e12}
+                del sw
+                torch.cuda.empty_cache()
+            sweep[str(n)] = row
+        res["prefill_llama_sweep"] = sweep
 
     if not args.no_prefill and not args.no_precision:
         # the other precision assignments of the PV product (Sec. 3.1, Fig. 3a)
