@@ -88,6 +88,8 @@ def parse():
     ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant runs")
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed serving step (separate launches vs one fused launch)")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the measurement of achievable GEMM and copy rates on this GPU")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the Llama-shaped prefill length sweep (16K, 32K, 64K tokens)")
     ap.add_argument("--no-precision", action="store_true",
@@ -119,6 +121,51 @@ class Timer:
     def ms(self):
         self.e.synchronize()
         return self.s.elapsed_time(self.e)
+
+
+def measured_peaks(torch):
+    """Achievable rates of this GPU, as a second denominator beside the
+    specification: large square GEMMs through torch (hipBLASLt) in FP16, BF16
+    and, where torch offers it, FP8 E4M3 with unit scales; and a 1 GiB device
+    copy (bytes read + written per second).  Context for the rooflines, not a
+    product path."""
+    out = {}
+    n = 8192
+
+    def timed(fn, reps=10):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        with Timer(torch) as t:
+            for _ in range(reps):
+                fn()
+        return t.ms() / reps
+
+    for name, dt in (("fp16_gemm_tflops", torch.float16), ("bf16_gemm_tflops", torch.bfloat16)):
+        a = torch.randn(n, n, device="cuda").to(dt)
+        b = torch.randn(n, n, device="cuda").to(dt)
+        ms = timed(lambda: torch.matmul(a, b))
+        out[name] = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+        del a, b
+    try:
+        a = torch.randn(n, n, device="cuda").to(torch.float8_e4m3fn)
+        b = torch.randn(n, n, device="cuda").to(torch.float8_e4m3fn).t()
+        one = torch.ones((), device="cuda")
+        ms = timed(lambda: torch._scaled_mm(a, b, scale_a=one, scale_b=one, out_dtype=torch.bfloat16))
+        out["fp8_gemm_tflops"] = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+        del a, b
+    except Exception as e:   # FP8 GEMM not available in this torch build
+        out["fp8_gemm_tflops"] = None
+        out["fp8_gemm_note"] = f"unavailable: {type(e).__name__}"
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    ms = timed(lambda: dst.copy_(src), reps=5)
+    out["copy_GBps"] = 2.0 * (1 << 30) / (ms * 1e-3) / 1e9
+    out["note"] = ("library rates on this stack (torch.matmul / _scaled_mm through hipBLASLt, "
+                   "8192^3; torch copy_ of 1 GiB, read + write bytes), not hardware peaks")
+    del src, dst
+    torch.cuda.empty_cache()
+    return out
 
 
 def setup_prefill(torch, np, mp, W, seq, smooth, mx=False, pv=0, wl=None):
@@ -619,6 +666,18 @@ def main():
         res["mixed_step"] = res_m
         del mx
         torch.cuda.empty_cache()
+
+    if not args.no_peaks:
+        log("achievable GEMM and copy rates ...")
+        pk = measured_peaks(torch)
+        res["measured_peaks"] = pk
+        if "prefill" in res and pk.get("fp16_gemm_tflops") and pk.get("fp8_gemm_tflops"):
+            # time-weighted over the two contractions of the exact-NVFP4 path
+            fl = res["prefill"]["flop"]
+            t_meas = (fl / 2) / (pk["fp16_gemm_tflops"] * 1e12) + (fl / 2) / (pk["fp8_gemm_tflops"] * 1e12)
+            res["roofline"]["frac_of_library_gemm"] = res["prefill"]["tflops"] * 1e12 / (fl / t_meas)
+        if "decode" in res and pk.get("copy_GBps"):
+            res["decode"]["frac_of_device_copy"] = res["decode"]["GB/s"] / pk["copy_GBps"]
 
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
