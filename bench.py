@@ -195,13 +195,13 @@ def run_prefill(mp, st):
                st["pt_d"], st["out"], st["q"].shape[0], st["flags"])
 
 
-def setup_decode(torch, np, mp, W, batch, mx=False):
+def setup_decode(torch, np, mp, W, batch, mx=False, smooth=True):
     wl = W.llama_decode(batch)
     dev = "cuda"
-    fmt = mp.MXFP4 if mx else 0
+    fmt = (mp.MXFP4 if mx else 0) | (mp.SMOOTH if smooth else 0)
     lens = wl.kv_len
     pt, n_pages = W.make_pages(wl.seed, lens)
-    cache = mp.PagedCache(n_pages, wl.h_q, wl.h_kv, dev)
+    cache = mp.PagedCache(n_pages, wl.h_q, wl.h_kv, dev, smooth=smooth)
     stats = mp.SeqStats(batch, wl.h_q, wl.h_kv, dev)
     d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
     # context cache write per sequence (statistics over the context, then frozen)
@@ -212,7 +212,7 @@ def setup_decode(torch, np, mp, W, batch, mx=False):
         qq = mp.QuantQ(ctx, 1, wl.h_q, dev)
         slots = W.slots_for(pt, b, range(ctx))
         mp.quantize_qk(q, k, v, d(np.array([0, ctx], np.int32)), d(slots), cache, sb, qq,
-                       mp.SMOOTH | mp.COMPUTE_STATS | fmt, ctx)
+                       mp.COMPUTE_STATS | fmt, ctx)
         stats.q_mean[b].copy_(sb.q_mean[0])
         stats.k_mean[b].copy_(sb.k_mean[0])
         stats.k_tscale[b].copy_(sb.k_tscale[0])
@@ -224,7 +224,7 @@ def setup_decode(torch, np, mp, W, batch, mx=False):
     slots1 = np.array([W.slots_for(pt, b, [lens[b] - 1])[0] for b in range(batch)], np.int64)
     qq = mp.QuantQ(batch, batch, wl.h_q, dev)
     mp.quantize_qk(qn, kn, vn, d(np.arange(batch + 1, dtype=np.int32)), d(slots1), cache,
-                   stats, qq, mp.SMOOTH | fmt, 1)
+                   stats, qq, fmt, 1)
     part = mp.decode_choose_partition(lens, wl.h_kv, torch.cuda.get_device_properties(0).multi_processor_count)
     maxp = max(math.ceil(n / part) for n in lens)
     ws = torch.empty(mp.decode_workspace_size(batch, wl.h_q, maxp) // 4, dtype=torch.float32,
@@ -233,7 +233,7 @@ def setup_decode(torch, np, mp, W, batch, mx=False):
     torch.cuda.synchronize()
     return dict(wl=wl, lens=lens, pt=pt, pt_d=d(pt), cache=cache, stats=stats, qq=qq, ws=ws,
                 out=out, kv_len=d(np.asarray(lens, np.int32)), part=part, maxp=maxp,
-                flags=mp.SMOOTH | fmt, mx=mx)
+                flags=fmt, mx=mx, smooth=smooth)
 
 
 def run_decode(mp, st):
@@ -243,11 +243,12 @@ def run_decode(mp, st):
 
 def decode_bytes(st):
     """Algorithmic bytes of one decode launch: K codes + scales + V codes + Delta_S of
-    every key, the quantized queries, the outputs, the page-table entries."""
+    every key (none without smoothing), the quantized queries, the outputs, the
+    page-table entries."""
     wl = st["wl"]
     keys = sum(st["lens"])
     scale_bytes = 4 if st.get("mx") else 8       # MXFP4 reads scale bytes 0..3 only
-    per_key = wl.h_kv * (64 + scale_bytes + 128) + wl.h_q * 2
+    per_key = wl.h_kv * (64 + scale_bytes + 128) + (wl.h_q * 2 if st.get("smooth", True) else 0)
     pages = sum(math.ceil(n / 64) for n in st["lens"])
     return keys * per_key + wl.batch * wl.h_q * (72 + 4) + wl.batch * wl.h_q * 256 + pages * 4 \
         + wl.batch * 4
@@ -626,6 +627,28 @@ def main():
                          "keys": int(sum(sd["lens"]))}
         del sd
         torch.cuda.empty_cache()
+        if not args.no_direct:
+            # the direct variant reads no Delta_S side cache (Sec. 7.2 puts that
+            # cache at about 4 % of the KV bytes)
+            log("decode, direct (unsmoothed) variant ...")
+            sdd = setup_decode(torch, np, mp, W, args.decode_batch, smooth=False)
+            for _ in range(args.warmup):
+                run_decode(mp, sdd)
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(args.steps):
+                with Timer(torch) as t:
+                    run_decode(mp, sdd)
+                ts.append(t)
+            torch.cuda.synchronize()
+            dd_ms = sum(t.ms() for t in ts) / args.steps
+            dd_bytes = decode_bytes(sdd)
+            res["decode"]["direct_ms"] = dd_ms
+            res["decode"]["direct_GB/s"] = dd_bytes / (dd_ms * 1e-3) / 1e9
+            res["decode"]["smoothing_overhead"] = decode_ms / dd_ms - 1.0
+            res["decode"]["side_cache_byte_share"] = 1.0 - dd_bytes / nbytes
+            del sdd
+            torch.cuda.empty_cache()
         if not args.no_mxfp4:
             log("decode, MXFP4 variant ...")
             sx = setup_decode(torch, np, mp, W, args.decode_batch, mx=True)
