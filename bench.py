@@ -88,6 +88,8 @@ def parse():
     ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant runs")
     ap.add_argument("--no-mixed", action="store_true",
                     help="skip the mixed serving step (separate launches vs one fused launch)")
+    ap.add_argument("--no-decode128k", action="store_true",
+                    help="skip the decode batch whose contexts are all 131072 tokens")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip the measurement of achievable GEMM and copy rates on this GPU")
     ap.add_argument("--no-sweep", action="store_true",
@@ -195,8 +197,8 @@ def run_prefill(mp, st):
                st["pt_d"], st["out"], st["q"].shape[0], st["flags"])
 
 
-def setup_decode(torch, np, mp, W, batch, mx=False, smooth=True):
-    wl = W.llama_decode(batch)
+def setup_decode(torch, np, mp, W, batch, mx=False, smooth=True, ctx_range=None):
+    wl = W.llama_decode(batch) if ctx_range is None else W.llama_decode(batch, *ctx_range)
     dev = "cuda"
     fmt = (mp.MXFP4 if mx else 0) | (mp.SMOOTH if smooth else 0)
     lens = wl.kv_len
@@ -648,6 +650,27 @@ def main():
             res["decode"]["smoothing_overhead"] = decode_ms / dd_ms - 1.0
             res["decode"]["side_cache_byte_share"] = 1.0 - dd_bytes / nbytes
             del sdd
+            torch.cuda.empty_cache()
+        if not args.no_decode128k:
+            # every context at 131072 tokens: the "128K decode" point of the target
+            log("decode, batch of 131072-token contexts ...")
+            s128 = setup_decode(torch, np, mp, W, args.decode_batch, ctx_range=(131072, 131072))
+            for _ in range(args.warmup):
+                run_decode(mp, s128)
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(args.steps):
+                with Timer(torch) as t:
+                    run_decode(mp, s128)
+                ts.append(t)
+            torch.cuda.synchronize()
+            d128_ms = sum(t.ms() for t in ts) / args.steps
+            d128_bytes = decode_bytes(s128)
+            res["decode_128k"] = {"ms": d128_ms, "GB/s": d128_bytes / (d128_ms * 1e-3) / 1e9,
+                                  "frac_hbm": d128_bytes / (d128_ms * 1e-3) / PEAK_HBM,
+                                  "bytes": d128_bytes, "partition_tokens": s128["part"],
+                                  "contexts": f"{args.decode_batch} x 131072"}
+            del s128
             torch.cuda.empty_cache()
         if not args.no_mxfp4:
             log("decode, MXFP4 variant ...")

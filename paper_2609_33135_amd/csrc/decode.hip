@@ -38,7 +38,15 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeParams p) {
 
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
   if (p.batch == 0) return hipSuccess;
-  const dim3 grid((p.max_partitions + kWavesPerBlock - 1) / kWavesPerBlock, p.h_kv, p.batch);
+  // Workgroups are dealt to the 8 XCDs round-robin by linear block id.  With
+  // an even number of partition groups per (KV head, sequence) row the XCD of
+  // a block depends mostly on its partition group, and the late groups exist
+  // only for the long sequences, so the XCDs get unequal work (0.95 ms
+  // against 0.84 ms for the Llama batch when the count is a multiple of 8).
+  // An odd count spreads every row over all XCDs; the extra groups hold no
+  // partition of any sequence and return at once.
+  const int groups = (p.max_partitions + kWavesPerBlock - 1) / kWavesPerBlock;
+  const dim3 grid(groups | 1, p.h_kv, p.batch);
   const dim3 block(kWavesPerBlock * 64);
   if (p.mx) {
     if (p.smooth) decode_kernel<true, true><<<grid, block, 0, stream>>>(p);
