@@ -182,6 +182,13 @@ static mpfa_status decode_params(const mpfa_decode_args* a, void* workspace, siz
   if (a->h_q / a->h_kv > kMaxDecodeGroup) return MPFA_ERR_UNSUPPORTED;
   if (a->flags & (MPFA_PV_BF16 | MPFA_PV_NVFP4)) return MPFA_ERR_UNSUPPORTED;
   if (a->flags & ~(MPFA_SMOOTH | MPFA_MXFP4)) return MPFA_ERR_INVALID;
+  {
+    // the decode grid is one dimension of 256-thread workgroups: per
+    // (sequence, group of 4 partitions) pair, the KV heads rounded up to 8
+    const int64_t groups = (a->max_partitions + 3) / 4;
+    const int64_t blocks = (int64_t)a->batch * groups * ((a->h_kv + 7) / 8 * 8);
+    if (blocks * 256 > (int64_t)UINT32_MAX) return MPFA_ERR_UNSUPPORTED;
+  }
   const bool smooth = a->flags & MPFA_SMOOTH;
   if (!a->kv_len || !a->page_table || !a->q_codes || !a->q_scales || !a->q_tscale ||
       !a->k_codes || !a->k_scales || !a->v_codes || !a->k_tscale || !a->out || (smooth && !a->ds))

@@ -19,12 +19,51 @@ namespace mpfa {
 
 namespace {
 
+// Block -> work map.  Workgroups are dealt to the 8 XCDs round-robin by block
+// id.  The (sequence, group of kWavesPerBlock partitions) pairs that hold work
+// are numbered k = 0, 1, ... in sequence order, so no workgroup is spent on a
+// partition past a short sequence's end.  Pair k takes the 8 blocks of slot k
+// (one per XCD), and the KV head run on XCD x is (x - k) mod 8: each pair's
+// heads spread over all XCDs and every XCD sees every head, so the XCDs share
+// the work evenly whatever the sequence lengths.  KV head counts above 8 take
+// ceil(h_kv / 8) consecutive slots per pair.  A block finds its pair by a
+// prefix sum of the sequences' group counts across the wave's lanes, 64
+// sequences at a time.
+__device__ __forceinline__ int partition_groups(int kvl, int partition_tokens) {
+  const int np = (kvl + partition_tokens - 1) / partition_tokens;
+  return (np + kWavesPerBlock - 1) / kWavesPerBlock;
+}
+
 template <bool SMOOTH, bool MX>
 __global__ __launch_bounds__(kWavesPerBlock * 64, 2) void decode_kernel(DecodeParams p) {
   __shared__ __attribute__((aligned(16))) uint8_t vlds[kWavesPerBlock * kVBytes];
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int hrows = (p.h_kv + 7) >> 3;
+  const int k = slot / hrows, hk = (slot % hrows) * 8 + ((xcd - k) & 7);
+  if (hk >= p.h_kv) return;
+  const int lane = threadIdx.x & 63;
+  int b = -1, grp = 0, base = 0;
+  for (int b0 = 0; b0 < p.batch && b < 0; b0 += 64) {
+    const int bb = b0 + lane;
+    const int cnt = bb < p.batch ? partition_groups(p.kv_len[bb], p.partition_tokens) : 0;
+    int incl = cnt;   // inclusive prefix sum over the lanes
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int up = __shfl_up(incl, d);
+      if (lane >= d) incl += up;
+    }
+    const int total = __shfl(incl, 63);
+    if (k < base + total) {
+      const uint64_t past = __ballot(base + incl > k);   // lanes whose sequence ends after pair k
+      const int first = __ffsll((unsigned long long)past) - 1;
+      b = b0 + first;
+      grp = k - (base + __shfl(incl, first) - __shfl(cnt, first));
+    }
+    base += total;
+  }
+  if (b < 0) return;   // the grid is sized for batch * ceil(max_partitions / 4) pairs
   const int wave = threadIdx.x >> 6;
-  decode_partition<SMOOTH, MX, false>(p, blockIdx.z, blockIdx.y, blockIdx.x * kWavesPerBlock + wave,
-                                      vlds + wave * kVBytes, nullptr);
+  decode_partition<SMOOTH, MX, false>(p, b, hk, grp * kWavesPerBlock + wave, vlds + wave * kVBytes, nullptr);
 }
 
 // One workgroup (128 threads, one per channel) per (sequence, query head).
@@ -38,15 +77,10 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeParams p) {
 
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
   if (p.batch == 0) return hipSuccess;
-  // Workgroups are dealt to the 8 XCDs round-robin by linear block id.  With
-  // an even number of partition groups per (KV head, sequence) row the XCD of
-  // a block depends mostly on its partition group, and the late groups exist
-  // only for the long sequences, so the XCDs get unequal work (0.95 ms
-  // against 0.84 ms for the Llama batch when the count is a multiple of 8).
-  // An odd count spreads every row over all XCDs; the extra groups hold no
-  // partition of any sequence and return at once.
   const int groups = (p.max_partitions + kWavesPerBlock - 1) / kWavesPerBlock;
-  const dim3 grid(groups | 1, p.h_kv, p.batch);
+  const int64_t pairs = (int64_t)p.batch * groups;
+  const int64_t nblocks = pairs * ((p.h_kv + 7) / 8 * 8);
+  const dim3 grid((unsigned)nblocks);
   const dim3 block(kWavesPerBlock * 64);
   if (p.mx) {
     if (p.smooth) decode_kernel<true, true><<<grid, block, 0, stream>>>(p);

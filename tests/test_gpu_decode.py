@@ -121,6 +121,19 @@ def test_decode_medium_contexts(orc, mp):
     _cmp(run, part, "medium")
 
 
+@pytest.mark.parametrize("h_q,h_kv", [(24, 12), (4, 1)])
+def test_decode_many_sequences(orc, mp, h_q, h_kv):
+    """70 sequences (the device-side pair numbering scans 64 sequences at a
+    time), lengths from 1 to 700 with several one-partition sequences, and KV
+    head counts that are not a multiple of 8."""
+    print(f"case: decode 70 sequences {h_q}q/{h_kv}kv", flush=True)
+    rng = np.random.default_rng(79)
+    lens = rng.integers(1, 700, 70)
+    lens[[0, 5, 63, 64, 69]] = [1, 128, 129, 700, 2]
+    run = DecodeRun(orc, mp, 79, lens, h_q, h_kv)
+    _cmp(run, 128, f"70 seqs {h_q}/{h_kv}")
+
+
 def test_decode_matches_prefill_last_row(orc, mp):
     """With one partition covering the context, decode of the last token equals
     the last row of prefill over the same cache (same tiles, same order)."""
