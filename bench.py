@@ -170,6 +170,53 @@ def measured_peaks(torch):
     return out
 
 
+def probe_peaks(torch, mp):
+    """Achievable rates measured by the library's own probe kernels: each MFMA
+    form the attention kernels use, issued back to back by 8 waves per SIMD
+    (2048 workgroups, 8 independent accumulators per wave), and the HBM read
+    rate of a 4 GiB buffer read once through registers or directly into LDS,
+    each workgroup streaming a contiguous share (best of four grid sizes).
+    Best of 3 launches each, HIP events."""
+    out = {}
+    blocks, iters = 2048, 10000
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    for name, kind in (("mfma_f16_tflops", mp.PROBE_MFMA_F16), ("mfma_fp8_tflops", mp.PROBE_MFMA_FP8),
+                       ("mfma_fp4_tflops", mp.PROBE_MFMA_FP4)):
+        mp.probe_mfma(kind, 10, blocks, sink)
+        torch.cuda.synchronize()
+        best = None
+        for _ in range(3):
+            with Timer(torch) as t:
+                fl = mp.probe_mfma(kind, iters, blocks, sink)
+            ms = t.ms()
+            best = ms if best is None else min(best, ms)
+        out[name] = fl / (best * 1e-3) / 1e12
+    del sink
+    nbytes = 1 << 32
+    buf = torch.empty(nbytes // 4, dtype=torch.int32, device="cuda")
+    buf.fill_(0x5A5A5A5A)
+    for name, mode in (("read_vgpr_GBps", mp.PROBE_READ_VGPR), ("read_lds_GBps", mp.PROBE_READ_LDS)):
+        best, best_blocks = None, None
+        for nb in (1024, 2048, 4096, 8192):
+            sink = torch.empty(nb * 256, dtype=torch.int32, device="cuda")
+            mp.probe_read(mode, buf, nb, sink)
+            torch.cuda.synchronize()
+            for _ in range(3):
+                with Timer(torch) as t:
+                    mp.probe_read(mode, buf, nb, sink)
+                ms = t.ms()
+                if best is None or ms < best:
+                    best, best_blocks = ms, nb
+            del sink
+        out[name] = nbytes / (best * 1e-3) / 1e9
+        out[name.replace("GBps", "blocks")] = best_blocks
+    del buf
+    torch.cuda.empty_cache()
+    out["note"] = ("probe kernels of libmpfa (mpfa_probe_mfma, mpfa_probe_read): dense MFMA issue "
+                   "rate per form and single-pass HBM read rate")
+    return out
+
+
 def setup_prefill(torch, np, mp, W, seq, smooth, mx=False, pv=0, wl=None):
     wl = wl if wl is not None else W.qwen_prefill(seq)
     dev = "cuda"
@@ -724,6 +771,25 @@ def main():
             res["roofline"]["frac_of_library_gemm"] = res["prefill"]["tflops"] * 1e12 / (fl / t_meas)
         if "decode" in res and pk.get("copy_GBps"):
             res["decode"]["frac_of_device_copy"] = res["decode"]["GB/s"] / pk["copy_GBps"]
+        log("probe kernels: MFMA issue rates and HBM read rate ...")
+        pp = probe_peaks(torch, mp)
+        res["measured_peaks"]["probe"] = pp
+        if "prefill" in res:
+            # the same time weighting as the specification peaks: half the FLOP in
+            # each contraction
+            hm = lambda a, b: 2.0 / (1.0 / a + 1.0 / b)
+            meas_fp4_fp8 = hm(pp["mfma_fp4_tflops"], pp["mfma_fp8_tflops"])
+            meas_f16_fp8 = hm(pp["mfma_f16_tflops"], pp["mfma_fp8_tflops"])
+            res["roofline"]["measured_peak"] = meas_fp4_fp8
+            res["roofline"]["frac_of_measured_peak"] = res["prefill"]["tflops"] / meas_fp4_fp8
+            res["roofline"]["measured_exact_path_peak"] = meas_f16_fp8
+            res["roofline"]["frac_of_measured_exact_path_peak"] = res["prefill"]["tflops"] / meas_f16_fp8
+        if "decode" in res:
+            read = max(pp["read_vgpr_GBps"], pp["read_lds_GBps"])
+            res["decode"]["frac_of_measured_read"] = res["decode"]["GB/s"] / read
+        if "decode_128k" in res:
+            res["decode_128k"]["frac_of_measured_read"] = res["decode_128k"]["GB/s"] / max(
+                pp["read_vgpr_GBps"], pp["read_lds_GBps"])
 
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")

@@ -14,7 +14,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmpfa.so")
 
-SOURCES = ["api.cpp", "quantize.hip", "prefill.hip", "decode.hip", "mixed.hip", "debug_checks.hip"]
+SOURCES = ["api.cpp", "quantize.hip", "prefill.hip", "decode.hip", "mixed.hip", "debug_checks.hip", "probe.hip"]
 DEBUG_LIB = os.path.join(PKG, "libmpfa_debug.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CLANG = os.environ.get("MPFA_CLANG", "/opt/rocm/lib/llvm/bin/clang++")
@@ -32,7 +32,10 @@ COMMON = [
 # them).  Without NaN semantics fmaxf over MFMA results needs no quieting
 # v_max_f32 per operand, which takes about 70 VALU instructions out of every
 # 128-key tile of the prefill loop.
-EXTRA = {"prefill.hip": ["-fno-honor-nans"], "mixed.hip": ["-fno-honor-nans"]}
+EXTRA = {"prefill.hip": ["-fno-honor-nans"], "mixed.hip": ["-fno-honor-nans"],
+         # the MFMA probe keeps its accumulators in VGPRs: with the AGPR form the
+         # compiler copies them between the two register files inside the loop
+         "probe.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src: str, debug: bool = False) -> str:

@@ -168,3 +168,19 @@ def test_mixed_step_validation(mp):
     pa.flags, da.flags = 1, 1
     assert mp.lib().mpfa_mixed_step(C.byref(pa), C.byref(da), 0x1000, states, None) == 3
     assert mp.lib().mpfa_mixed_step(None, C.byref(da), 0x1000, 1 << 30, None) == 1
+
+
+def test_probe_validation(mp):
+    """The measurement probes reject bad arguments on the host; the fake device
+    addresses below are never dereferenced."""
+    L = mp.lib()
+    sink = 0x1000
+    for kind, iters, blocks, s in ((3, 1, 1, sink), (-1, 1, 1, sink), (0, 0, 1, sink), (0, 1, 0, sink),
+                                   (0, 1, (1 << 20) + 1, sink), (0, 1, 1, None)):
+        assert L.mpfa_probe_mfma(kind, iters, blocks, 0, 0, s, None) == 1, (kind, iters, blocks)
+    per_round = 4 * 256 * 8 * 16
+    for mode, src, nbytes, blocks, s in ((2, 0x1000, per_round, 4, sink), (0, None, per_round, 4, sink),
+                                         (0, 0x1008, per_round, 4, sink), (0, 0x1000, per_round + 16, 4, sink),
+                                         (0, 0x1000, 0, 4, sink), (0, 0x1000, per_round, 0, sink),
+                                         (1, 0x1000, per_round, 4, None)):
+        assert L.mpfa_probe_read(mode, src, nbytes, blocks, s, None) == 1, (mode, src, nbytes, blocks)
