@@ -465,8 +465,8 @@ def cpu_baseline(np, W, st, rows):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is "
-                                   "described in DESIGN.md but not built"}))
+        print(json.dumps({"error": "one GPU only: the kernels run on a single MI355X; sharding heads "
+                                   "or sequences across GPUs is not built"}))
         sys.exit(2)
     import torch
     import paper_2609_33135_amd as mp
