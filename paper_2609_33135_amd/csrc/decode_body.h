@@ -122,10 +122,16 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
   u32x4 kc[8];
   uint32_t ksc[8];
   uint2 dsw[8];
-  auto load_k = [&](int j) {
-    const int64_t pg0 = pt[min(2 * j, npg - 1)];
-    const int64_t pg1 = pt[min(2 * j + 1, npg - 1)];
-    const int64_t kpage = (lr < 8) ? pg0 : pg1;     // MFMA rows 0..7 hold keys 0..63
+  // The pages of tile j that the lane reads: its K rows' page (MFMA rows 0..7
+  // hold keys 0..63) and its V / Delta_S page (lane groups 0, 1: keys 0..63).
+  // They are loaded one tile ahead of their use, so no address computation
+  // waits on a page-table load (a dependent load would drain every load the
+  // wave has in flight); as per-lane values they stay in vector registers.
+  auto tile_pages = [&](int j, int& kp, int& vp) {
+    kp = pt[min(2 * j + (lr >> 3), npg - 1)];
+    vp = pt[min(2 * j + (g >> 1), npg - 1)];
+  };
+  auto load_k = [&](int64_t kpage, int64_t dpage) {
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb) {
       const int64_t row = kpage * page_k_rows + kv_head + ((krow_in_tile + 4 * mb) & 63);
@@ -135,7 +141,6 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
     }
     // compensation of the lane's accumulator rows: keys 32g + 4mb .. +3, head lr
     if (SMOOTH) {
-      const int64_t dpage = (g < 2) ? pg0 : pg1;
       const uint16_t* dsp = p.ds + (dpage * p.h_q + h) * kPage + ((32 * g) & 63);
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) dsw[mb] = *reinterpret_cast<const uint2*>(dsp + 4 * mb);
@@ -145,8 +150,7 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
     }
   };
   // ---- V tile j: 16 direct global->LDS loads of 16 bytes per lane
-  auto load_v = [&](int j) {
-    const int64_t vpage = pt[min(2 * j + (g >> 1), npg - 1)];
+  auto load_v = [&](int64_t vpage) {
     const uint8_t* vsrc = p.v_codes + ((vpage * p.h_kv + hk) * kD + lr) * kPage + ((32 * g) & 63);
 #pragma unroll
     for (int db = 0; db < 8; ++db)
@@ -199,14 +203,17 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
   };
 
   const int j_lo = kbeg / kTile, j_hi = (kend - 1) / kTile;
-  load_k(j_hi);
+  int cur_k, cur_v, nxt_k = 0, nxt_v = 0;   // the lane's pages of tile j, of tile j - 1
+  tile_pages(j_hi, cur_k, cur_v);
+  load_k(cur_k, cur_v);
+  tile_pages(max(j_hi - 1, j_lo), nxt_k, nxt_v);
   for (int j = j_hi; j >= j_lo; --j) {
     const int key0 = j * kTile;
     __builtin_amdgcn_s_waitcnt(0);   // K(j) in registers, V(j+1) in LDS
     if (pv_tile >= 0) pv();
     // the LDS reads of PV(j+1) must be complete before V(j) overwrites them
     __builtin_amdgcn_s_waitcnt(0);
-    load_v(j);
+    load_v(cur_v);
     // ---- S^T = 1 Delta_S^T + K Q^T (the rank-G term as accumulator input)
     f32x4 s[8];
 #pragma unroll
@@ -224,7 +231,12 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
         s[mb] = mfma_f16(dequant8(kc[mb][3], s1), qop[3], c);
       }
     }
-    if (j > j_lo) load_k(j - 1);
+    if (j > j_lo) load_k(nxt_k, nxt_v);
+    // outside the branch: copying a page index inside it would make the
+    // compiler wait for the K loads at the join
+    cur_k = nxt_k;
+    cur_v = nxt_v;
+    tile_pages(max(j - 2, j_lo), nxt_k, nxt_v);
     if (key0 + kTile > kend) {
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb)
