@@ -243,9 +243,9 @@ mpfa_status mpfa_prefill(const mpfa_prefill_args* args, mpfa_stream_t stream);
  * partition (GQA packing); the compensation becomes a rank-G seed.
  * workspace: caller-owned device memory of at least
  * mpfa_decode_workspace_size(...) bytes; its contents on entry are ignored.
- * Launch limit: batch * ceil(max_partitions / 4) * (h_kv rounded up to 8)
- * workgroups of 256 threads must stay below 2^32 threads, else
- * MPFA_ERR_UNSUPPORTED.
+ * Launch limit: for batch <= 512, batch * ceil(max_partitions / 4) * (h_kv
+ * rounded up to 8) workgroups of 256 threads must stay below 2^32 threads,
+ * else MPFA_ERR_UNSUPPORTED (larger batches use a three-dimensional grid).
  */
 typedef struct {
     int32_t batch, h_q, h_kv, head_dim;

@@ -183,10 +183,13 @@ static mpfa_status decode_params(const mpfa_decode_args* a, void* workspace, siz
   if (a->flags & (MPFA_PV_BF16 | MPFA_PV_NVFP4)) return MPFA_ERR_UNSUPPORTED;
   if (a->flags & ~(MPFA_SMOOTH | MPFA_MXFP4)) return MPFA_ERR_INVALID;
   {
-    // the decode grid is one dimension of 256-thread workgroups: per
-    // (sequence, group of 4 partitions) pair, the KV heads rounded up to 8
+    // up to kDecodePackedMaxBatch sequences the decode grid is one dimension of 256-thread
+    // workgroups: per (sequence, group of 4 partitions) pair, the KV heads
+    // rounded up to 8; above, its x dimension is the odd group count
     const int64_t groups = (a->max_partitions + 3) / 4;
-    const int64_t blocks = (int64_t)a->batch * groups * ((a->h_kv + 7) / 8 * 8);
+    const int64_t blocks = a->batch <= mpfa::kDecodePackedMaxBatch
+                               ? (int64_t)a->batch * groups * ((a->h_kv + 7) / 8 * 8)
+                               : (groups | 1);
     if (blocks * 256 > (int64_t)UINT32_MAX) return MPFA_ERR_UNSUPPORTED;
   }
   const bool smooth = a->flags & MPFA_SMOOTH;

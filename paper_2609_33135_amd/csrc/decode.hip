@@ -28,15 +28,27 @@ namespace {
 // the work evenly whatever the sequence lengths.  KV head counts above 8 take
 // ceil(h_kv / 8) consecutive slots per pair.  A block finds its pair by a
 // prefix sum of the sequences' group counts across the wave's lanes, 64
-// sequences at a time.
+// sequences at a time.  That lookup costs every block O(batch), so batches
+// above kDecodePackedMaxBatch sequences use the plain grid (partition group, KV
+// head, sequence) instead, with an odd group count so that each (KV head,
+// sequence) row still spreads over the XCDs.  Either map gives every
+// partition to exactly one wave; the results do not depend on it.
 __device__ __forceinline__ int partition_groups(int kvl, int partition_tokens) {
   const int np = (kvl + partition_tokens - 1) / partition_tokens;
   return (np + kWavesPerBlock - 1) / kWavesPerBlock;
 }
 
-template <bool SMOOTH, bool MX>
+template <bool SMOOTH, bool MX, bool PACKED>
 __global__ __launch_bounds__(kWavesPerBlock * 64, 2) void decode_kernel(DecodeParams p) {
   __shared__ __attribute__((aligned(16))) uint8_t vlds[kWavesPerBlock * kVBytes];
+  const int wave = threadIdx.x >> 6;
+  if (!PACKED) {
+    // grid (partition group, KV head, sequence); groups past the sequence's
+    // partitions return inside decode_partition
+    decode_partition<SMOOTH, MX, false>(p, blockIdx.z, blockIdx.y, blockIdx.x * kWavesPerBlock + wave,
+                                        vlds + wave * kVBytes, nullptr);
+    return;
+  }
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
   const int hrows = (p.h_kv + 7) >> 3;
   const int k = slot / hrows, hk = (slot % hrows) * 8 + ((xcd - k) & 7);
@@ -62,7 +74,6 @@ __global__ __launch_bounds__(kWavesPerBlock * 64, 2) void decode_kernel(DecodePa
     base += total;
   }
   if (b < 0) return;   // the grid is sized for batch * ceil(max_partitions / 4) pairs
-  const int wave = threadIdx.x >> 6;
   decode_partition<SMOOTH, MX, false>(p, b, hk, grp * kWavesPerBlock + wave, vlds + wave * kVBytes, nullptr);
 }
 
@@ -78,16 +89,26 @@ __global__ __launch_bounds__(128) void merge_kernel(DecodeParams p) {
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
   if (p.batch == 0) return hipSuccess;
   const int groups = (p.max_partitions + kWavesPerBlock - 1) / kWavesPerBlock;
-  const int64_t pairs = (int64_t)p.batch * groups;
-  const int64_t nblocks = pairs * ((p.h_kv + 7) / 8 * 8);
-  const dim3 grid((unsigned)nblocks);
   const dim3 block(kWavesPerBlock * 64);
-  if (p.mx) {
-    if (p.smooth) decode_kernel<true, true><<<grid, block, 0, stream>>>(p);
-    else decode_kernel<false, true><<<grid, block, 0, stream>>>(p);
+  if (p.batch <= kDecodePackedMaxBatch) {
+    const int64_t pairs = (int64_t)p.batch * groups;
+    const dim3 grid((unsigned)(pairs * ((p.h_kv + 7) / 8 * 8)));
+    if (p.mx) {
+      if (p.smooth) decode_kernel<true, true, true><<<grid, block, 0, stream>>>(p);
+      else decode_kernel<false, true, true><<<grid, block, 0, stream>>>(p);
+    } else {
+      if (p.smooth) decode_kernel<true, false, true><<<grid, block, 0, stream>>>(p);
+      else decode_kernel<false, false, true><<<grid, block, 0, stream>>>(p);
+    }
   } else {
-    if (p.smooth) decode_kernel<true, false><<<grid, block, 0, stream>>>(p);
-    else decode_kernel<false, false><<<grid, block, 0, stream>>>(p);
+    const dim3 grid(groups | 1, p.h_kv, p.batch);
+    if (p.mx) {
+      if (p.smooth) decode_kernel<true, true, false><<<grid, block, 0, stream>>>(p);
+      else decode_kernel<false, true, false><<<grid, block, 0, stream>>>(p);
+    } else {
+      if (p.smooth) decode_kernel<true, false, false><<<grid, block, 0, stream>>>(p);
+      else decode_kernel<false, false, false><<<grid, block, 0, stream>>>(p);
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

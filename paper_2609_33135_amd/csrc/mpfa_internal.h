@@ -8,6 +8,10 @@
 namespace mpfa {
 
 constexpr int kMaxKvHeadsQuant = 32;
+// decode batches up to this many sequences use the packed, XCD-rotated block
+// map (each workgroup looks its work up with an O(batch) scan); larger ones a
+// three-dimensional grid
+constexpr int kDecodePackedMaxBatch = 512;
 
 struct QuantParams {
   int batch, total_tokens, max_seqlen, h_q, h_kv;

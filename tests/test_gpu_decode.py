@@ -134,6 +134,17 @@ def test_decode_many_sequences(orc, mp, h_q, h_kv):
     _cmp(run, 128, f"70 seqs {h_q}/{h_kv}")
 
 
+def test_decode_large_batch_grid(orc, mp):
+    """600 sequences: above 512 the kernel switches from the packed block map
+    to the three-dimensional grid; both must reach every partition once."""
+    print("case: decode 600 sequences 8q/2kv", flush=True)
+    rng = np.random.default_rng(83)
+    lens = rng.integers(1, 400, 600)
+    lens[[0, 511, 512, 599]] = [1, 399, 129, 257]
+    run = DecodeRun(orc, mp, 83, lens, 8, 2)
+    _cmp(run, 128, "600 seqs 8/2")
+
+
 def test_decode_matches_prefill_last_row(orc, mp):
     """With one partition covering the context, decode of the last token equals
     the last row of prefill over the same cache (same tiles, same order)."""
