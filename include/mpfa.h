@@ -134,7 +134,7 @@ typedef enum {
  *    call's tokens (Eq. 7), summed in FP32 sequentially inside 128-token
  *    blocks and then over the block partials in order, divided in FP32 and
  *    rounded to BF16 (written to q_mean / k_mean; zero without MPFA_SMOOTH);
- *    k_tscale[b][h] = smallest 2^k (k in [-64, 64]) with 2688 * 2^k >= max
+ *    k_tscale[b][h] = smallest 2^k (k in [-63, 63]) with 2688 * 2^k >= max
  *    |K - Kbar| over the call's tokens (1 if that max is 0 or with
  *    MPFA_TSCALE_UNIT).  Without the flag the means and k_tscale are read
  *    (frozen after the first prefill, Sec. 6).

@@ -164,7 +164,9 @@ void orc_bf16_encode_f32_array(const float* x, int64_t n, uint16_t* out)
 
 /* Second-level scale of NVFP4: a power of two chosen so that the largest
  * group scale amax/(6t) lands in (224, 448], i.e. the smallest t = 2^k with
- * 6 * 448 * t >= amax.  A power of two keeps every fold of t exact. */
+ * 6 * 448 * t >= amax.  A power of two keeps every fold of t exact.  k is
+ * clamped to [-63, 63] so that the product of a query and a key tensor scale,
+ * and its inverse, stay normal FP32 numbers (2^-126 .. 2^126). */
 float orc_tensor_scale(float amax)
 {
     if (!(amax > 0.0f)) return 1.0f;
@@ -173,8 +175,8 @@ float orc_tensor_scale(float amax)
     /* correct any log2 rounding with exact comparisons */
     while (k > -200 && ldexp(2688.0, k - 1) >= a) --k;
     while (ldexp(2688.0, k) < a) ++k;
-    if (k < -64) k = -64;
-    if (k > 64) k = 64;
+    if (k < -63) k = -63;
+    if (k > 63) k = 63;
     return (float)ldexp(1.0, k);
 }
 

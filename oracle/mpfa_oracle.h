@@ -81,8 +81,8 @@ void orc_bf16_encode_f32_array(const float* x, int64_t n, uint16_t* out);
 void orc_stats_one(const uint16_t* x, int64_t n_tok, int64_t stride, int smooth,
                    int tscale_unit, uint16_t* mean_out, float* tscale_out);
 
-/* Smallest power of two t = 2^k (k clamped to [-64, 64]) with 2688 * t >= amax;
- * 1 when amax == 0. */
+/* Smallest power of two t = 2^k (k clamped to [-63, 63], so that tQ * tK and
+ * its inverse are normal FP32 numbers) with 2688 * t >= amax; 1 when amax == 0. */
 float orc_tensor_scale(float amax);
 
 /* NVFP4 quantization of one 128-channel row of centered FP32 values:

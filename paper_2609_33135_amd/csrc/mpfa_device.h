@@ -77,16 +77,18 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_floa
 // floor(log2 |x|) for finite nonzero x (v_frexp_exp returns it plus one).
 __device__ __forceinline__ int ilog2f(float x) { return __builtin_amdgcn_frexp_expf(x) - 1; }
 
-// Second-level NVFP4 scale: smallest 2^k, k in [-64, 64], with 2688 * 2^k >= amax
+// Second-level NVFP4 scale: smallest 2^k, k in [-63, 63], with 2688 * 2^k >= amax
 // (so the largest group scale amax / (6 t) is at most 448); 1 when amax == 0.
+// The range keeps tQ * tK and its inverse normal FP32 numbers (2^-126 .. 2^126),
+// which the attention kernels fold into lambda and the compensation scale.
 __device__ __forceinline__ float tensor_scale(float amax) {
   if (!(amax > 0.0f)) return 1.0f;
   int e = ilog2f(amax);                    // amax in [2^e, 2^(e+1))
   int k = e - 12;
-  while (k < 64 && __builtin_ldexpf(2688.0f, k) < amax) ++k;
-  while (k > -64 && __builtin_ldexpf(2688.0f, k - 1) >= amax) --k;
-  if (k < -64) k = -64;
-  if (k > 64) k = 64;
+  while (k < 63 && __builtin_ldexpf(2688.0f, k) < amax) ++k;
+  while (k > -63 && __builtin_ldexpf(2688.0f, k - 1) >= amax) --k;
+  if (k < -63) k = -63;
+  if (k > 63) k = 63;
   return __builtin_ldexpf(1.0f, k);
 }
 

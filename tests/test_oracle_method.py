@@ -55,10 +55,11 @@ def test_tensor_scale_closed_form(orc):
         t = orc.tensor_scale(a)
         assert math.frexp(t)[0] == 0.5                    # power of two
         k = math.frexp(t)[1] - 1
-        if -64 < k < 64:
+        if -63 < k < 63:
             assert 2688.0 * t >= a and 1344.0 * t < a     # smallest such power
         else:                                             # clamped exponent range
-            assert (k == -64 and 2688.0 * t >= a) or (k == 64 and 1344.0 * t < a)
+            assert (k == -63 and 2688.0 * t >= a) or (k == 63 and 1344.0 * t < a)
+        assert -63 <= k <= 63
     assert orc.tensor_scale(0.0) == 1.0
 
 
@@ -143,6 +144,62 @@ def test_stats_match_fp64_mean(orc):
     assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-6)
 
 
+def test_stats_summation_order(orc):
+    """The mean's FP32 sum runs token by token inside each 128-token block and
+    then over the block partials (the reading the oracle and the kernels
+    share).  Hand-worked with 2^24, where adding 1 is lost to rounding:
+    - [2^24, 1, -2^24]: 2^24 + 1 rounds to 2^24 (tie to even), minus 2^24
+      gives 0, so the mean is 0 (token order reversed would give 1/3);
+    - 130 tokens [2^24, 0 x 127 | 1, -2^24]: block partials 2^24 and
+      1 - 2^24 = -16777215 (exact), total 1, mean RN(1/130) = BF16 0x3bfc
+      (one flat running sum would lose the 1 and give 0)."""
+    x = np.zeros((3, 128), np.float32)
+    x[:, 0] = [2.0 ** 24, 1.0, -2.0 ** 24]
+    mean, _ = orc.stats_one(bf16_bits(x), smooth=True)
+    assert mean[0] == 0x0000
+    x = np.zeros((130, 128), np.float32)
+    x[0, 0], x[128, 0], x[129, 0] = 2.0 ** 24, 1.0, -2.0 ** 24
+    mean, _ = orc.stats_one(bf16_bits(x), smooth=True)
+    assert mean[0] == 0x3BFC and not mean[1:].any()
+
+
+def test_centering_is_translation_invariant(orc):
+    """Sec. 4.2 quantizes Q_c = Q - Qbar and K_c = K - Kbar.  Adding a per-channel
+    constant c to every token moves the mean by exactly c (all values here are
+    multiples of 1/16 below 16, so every BF16 value and FP32 partial sum is
+    exact), so with smoothing the codes, group scales and tensor scales of
+    c + x equal those of x (whose exact mean is 0), and the means equal c.
+    The x values are nonzero: -0 centers to -0 (a sign-bit code) while
+    c + (-0) - c is +0."""
+    rng = np.random.default_rng(44)
+    n, h_q, h_kv = 256, 2, 1
+    def pairs(h):
+        half = rng.integers(1, 65, (n // 2, h, 128)) * rng.choice([-1.0, 1.0], (n // 2, h, 128)) / 16.0
+        out = np.empty((n, h, 128))
+        out[0::2], out[1::2] = half, -half
+        return out
+    xq, xk = pairs(h_q), pairs(h_kv)
+    cq = rng.integers(-80, 81, (1, h_q, 128)) / 16.0
+    ck = rng.integers(-80, 81, (1, h_kv, 128)) / 16.0
+    v = bf16_bits(rng.standard_normal((n, h_kv, 128)).astype(np.float32))
+    slots = np.arange(n, dtype=np.int64)
+    flags = orc.SMOOTH | orc.COMPUTE_STATS
+    base = orc.quantize_qk(bf16_bits(xq), bf16_bits(xk), v, [0, n], slots, 4, flags)
+    moved = orc.quantize_qk(bf16_bits(xq + cq), bf16_bits(xk + ck), v, [0, n], slots, 4, flags)
+    assert not base["q_mean"].any() and not base["k_mean"].any()
+    assert np.array_equal(bits_to_f64(moved["q_mean"]).reshape(1, h_q, 128), cq)
+    assert np.array_equal(bits_to_f64(moved["k_mean"]).reshape(1, h_kv, 128), ck)
+    for key in ("q_codes", "q_scales", "q_tscale", "k_tscale"):
+        assert np.array_equal(base[key], moved[key]), key
+    for key in ("k_codes", "k_scales", "v_codes"):
+        assert np.array_equal(base["cache"][key], moved["cache"][key]), key
+    # without centering the translated input quantizes differently
+    direct = orc.quantize_qk(bf16_bits(xq + cq), bf16_bits(xk + ck), v, [0, n], slots, 4,
+                             orc.COMPUTE_STATS)
+    assert not np.array_equal(direct["q_codes"], base["q_codes"])
+    assert not np.array_equal(direct["cache"]["k_codes"], base["cache"]["k_codes"])
+
+
 def _quant_small(orc, seed, n, h_q=1, h_kv=1, flags=None, zero_mean=False, outliers=False):
     q = W.gen_tensor(seed, W.STREAM_Q, 0, 0, n, h_q, outliers=outliers, out_stream=W.STREAM_OUT_Q)
     off = W.k_offsets(seed, h_kv)
@@ -194,6 +251,96 @@ def test_zero_mean_input_makes_compensation_vanish(orc):
     b, _ = orc.prefill(off["cache"], pt, [n], off["k_tscale"], off["q_codes"], off["q_scales"],
                        off["q_tscale"], [0, n], [0], items, smooth=False)
     assert np.array_equal(a, b)
+
+
+def test_delta_s_is_sequential_fp32_fma_chain(orc):
+    """Eq. 9 in the reading the kernels share: an FP32 fused multiply-add chain
+    over channels 0..127 starting from +0, then BF16.  Hand-worked: Qbar =
+    (1, 1, 1, 0, ...), K_c = +-(2^24, 1, -2^24, 0, ...) (two tokens, so Kbar = 0
+    exactly).  fma(1, 2^24, 0) = 2^24; fma(1, 1, 2^24) = 2^24 + 1 rounds to
+    2^24 (tie to even); fma(1, -2^24, 2^24) = +0.  Both keys give +0, where an
+    FP64 dot product gives +-1 and the channels summed last to first give 1."""
+    q = np.zeros((2, 1, 128), np.float32)
+    q[:, 0, :3] = 1.0
+    w = np.zeros(128, np.float32)
+    w[:3] = [2.0 ** 24, 1.0, -2.0 ** 24]
+    k = np.stack([w, -w])[:, None, :]
+    v = np.zeros((2, 1, 128), np.float32)
+    r = orc.quantize_qk(bf16_bits(q), bf16_bits(k), bf16_bits(v), [0, 2],
+                        np.arange(2, dtype=np.int64), 1, orc.SMOOTH | orc.COMPUTE_STATS)
+    assert np.array_equal(bits_to_f64(r["q_mean"][0, 0, :4]), [1, 1, 1, 0])
+    assert not r["k_mean"].any()
+    assert list(r["cache"]["ds"][0, 0, :2]) == [0x0000, 0x0000]
+
+
+def test_chunked_prefill_equals_rows_of_the_full_prefill(orc):
+    """A chunk of queries at absolute positions q_start .. q_start + n - 1 over
+    the cached keys (Sec. 6, chunked prefill) sees exactly the keys the same
+    rows see in one full prefill, so the outputs are bit-identical."""
+    n, p0, h_q = 300, 200, 2
+    qb, kb, vb, r = _quant_small(orc, 23, n, h_q=h_q, h_kv=1, outliers=True)
+    pt = np.arange(5, dtype=np.int32)[None]
+    full_items = np.array([(0, i, h) for i in range(p0, n) for h in range(h_q)], np.int32)
+    full, _ = orc.prefill(r["cache"], pt, [n], r["k_tscale"], r["q_codes"], r["q_scales"],
+                          r["q_tscale"], [0, n], [0], full_items)
+    chunk_items = np.array([(0, i, h) for i in range(n - p0) for h in range(h_q)], np.int32)
+    chunk, _ = orc.prefill(r["cache"], pt, [n], r["k_tscale"], r["q_codes"][p0:],
+                           r["q_scales"][p0:], r["q_tscale"], [0, n - p0], [p0], chunk_items)
+    assert np.array_equal(full, chunk)
+    # the same chunk placed at position 0 is a different computation
+    early, _ = orc.prefill(r["cache"], pt, [n], r["k_tscale"], r["q_codes"][p0:],
+                           r["q_scales"][p0:], r["q_tscale"], [0, n - p0], [0], chunk_items)
+    assert not np.array_equal(full, early)
+
+
+def test_power_of_two_rescaling_is_exact(orc):
+    """Q * 2^a and K * 2^-a (a power of two, no clamping) leave every NVFP4 code
+    and group scale unchanged, multiply t_Q by 2^a and t_K by 2^-a, leave
+    Delta_S = Qbar . K_c unchanged (exact power-of-two factors), and so give
+    bit-identical attention: the two tensor scales enter the scores as the
+    product t_Q t_K (Eq. 1 with the second-level scale)."""
+    n, h_q, h_kv, a = 256, 4, 2, 20
+    q, k, v = W.gen_qkv(29, [n], h_q, h_kv, True, "cpu")
+    slots = np.arange(n, dtype=np.int64)
+    flags = orc.SMOOTH | orc.COMPUTE_STATS
+    r0 = orc.quantize_qk(W.bits(q), W.bits(k), W.bits(v), [0, n], slots, 4, flags)
+    r1 = orc.quantize_qk(W.bits(q * 2.0 ** a), W.bits(k * 2.0 ** -a), W.bits(v), [0, n], slots, 4,
+                         flags)
+    for key in ("q_codes", "q_scales"):
+        assert np.array_equal(r0[key], r1[key]), key
+    for key in ("k_codes", "k_scales", "v_codes", "ds"):
+        assert np.array_equal(r0["cache"][key], r1["cache"][key]), key
+    assert np.array_equal(r1["q_tscale"], r0["q_tscale"] * np.float32(2.0 ** a))
+    assert np.array_equal(r1["k_tscale"], r0["k_tscale"] * np.float32(2.0 ** -a))
+    assert not np.array_equal(r0["q_tscale"][0, :h_kv], r0["k_tscale"][0])
+    pt = np.arange(4, dtype=np.int32)[None]
+    items = np.array([(0, i, h) for i in range(0, n, 7) for h in range(h_q)], np.int32)
+    outs = [orc.prefill(r["cache"], pt, [n], r["k_tscale"], r["q_codes"], r["q_scales"],
+                        r["q_tscale"], [0, n], [0], items)[0] for r in (r0, r1)]
+    assert np.array_equal(outs[0], outs[1])
+
+
+def test_tiny_heads_give_the_uniform_average(orc):
+    """Q and K near 1e-17: both tensor scales sit at the bottom of their range
+    (2^-63), every score is below 1e-30, so 2^(lambda (S - m)) is exactly 1 in
+    FP64, P_hat = 448 for every visible key, and each output row is the plain
+    average of the FP8 V values of its visible keys (Sec. 4.1 with equal
+    scores)."""
+    n, h_q, h_kv = 256, 2, 1
+    q, k, v = W.gen_qkv(37, [n], h_q, h_kv, True, "cpu")
+    tiny = 2.0 ** -60
+    r = orc.quantize_qk(W.bits(q * tiny), W.bits(k * tiny), W.bits(v), [0, n],
+                        np.arange(n, dtype=np.int64), 4, orc.SMOOTH | orc.COMPUTE_STATS)
+    assert np.all(r["q_tscale"] == np.float32(2.0 ** -63))
+    assert np.all(r["k_tscale"] == np.float32(2.0 ** -63))
+    items = np.array([(0, i, h) for i in range(0, n, 5) for h in range(h_q)], np.int32)
+    o16, _ = orc.prefill(r["cache"], np.arange(4, dtype=np.int32)[None], [n], r["k_tscale"],
+                         r["q_codes"], r["q_scales"], r["q_tscale"], [0, n], [0], items)
+    vq = v.float().to(torch.float8_e4m3fn).double()[:, 0]      # [n][128], the FP8 V values
+    csum = torch.cumsum(vq, 0)
+    rows = torch.from_numpy(items[:, 1].astype(np.int64))
+    want = (csum[rows] / (rows + 1).double()[:, None]).to(torch.bfloat16)
+    assert np.array_equal(o16, W.bits(want))
 
 
 # ---------------------------------------------------------------------------
@@ -322,6 +469,39 @@ def test_prefill_matches_dequantized_reference_and_page_shuffle(orc):
         ref = orc.attention_f64(qd[rows], kd, vd, np.tile(dsd, (len(rows), 1)), rows,
                                 tile=128, flags=orc.REVERSE | orc.QUANT_P)
         assert np.max(np.abs(a64[sel] - ref)) < 1e-12
+
+
+def test_prefill_two_kv_heads_matches_numpy_layout(orc):
+    """The cache layout read back in numpy with two KV heads and shuffled pages:
+    K row (page, kv head, slot), V row (page, kv head, channel, slot), Delta_S
+    (page, q head, slot), query head h on KV head h // 2 (GQA 4:2).  FP64
+    attention over those dequantized arrays equals the oracle's prefill."""
+    n, h_q, h_kv = 200, 4, 2
+    q, k, v = W.gen_qkv(43, [n], h_q, h_kv, True, "cpu")
+    perm = np.array([2, 0, 3, 1], np.int32)
+    slots = perm[np.arange(n) // 64].astype(np.int64) * 64 + np.arange(n) % 64
+    r = orc.quantize_qk(W.bits(q), W.bits(k), W.bits(v), [0, n], slots, 4,
+                        orc.SMOOTH | orc.COMPUTE_STATS)
+    c = r["cache"]
+    items = np.array([(0, i, h) for i in range(0, n, 9) for h in range(h_q)], np.int32)
+    _, got = orc.prefill(c, perm[None], [n], r["k_tscale"], r["q_codes"], r["q_scales"],
+                         r["q_tscale"], [0, n], [0], items)
+    e4m3 = np.array([orc.e4m3_value(i) for i in range(256)])
+    pg, sl = slots // 64, slots % 64
+    for h in range(h_q):
+        hk = h // 2
+        kd = np.stack([orc.nvfp4_dequant_row(c["k_codes"][pg[j], hk, sl[j]],
+                                             c["k_scales"][pg[j], hk, sl[j]],
+                                             r["k_tscale"][0, hk]) for j in range(n)])
+        vd = e4m3[c["v_codes"][pg, hk, :, sl]]                    # [n][128]
+        dsd = bits_to_f64(c["ds"][pg, h, sl])
+        sel = items[:, 2] == h
+        rows = items[sel, 1]
+        qd = np.stack([orc.nvfp4_dequant_row(r["q_codes"][i, h], r["q_scales"][i, h],
+                                             r["q_tscale"][0, h]) for i in rows])
+        ref = orc.attention_f64(qd, kd, vd, np.tile(dsd, (len(rows), 1)), rows, tile=128,
+                                flags=orc.REVERSE | orc.QUANT_P)
+        assert np.max(np.abs(got[sel] - ref)) < 1e-12, h
 
 
 def test_decode_equals_last_prefill_row(orc):
