@@ -23,7 +23,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-PEAK_FP4 = 10.0e15        # MI355X dense MXFP4 FLOP/s
+PEAK_FP4 = 10.1e15        # MI355X dense MXFP4 / FP4 FLOP/s (published)
 PEAK_FP8 = 5.0e15         # dense FP8
 PEAK_BF16 = 2.5e15        # dense BF16 / FP16
 PEAK_HBM = 8.0e12         # bytes/s
@@ -171,7 +171,7 @@ def measured_peaks(torch):
 
 
 def probe_peaks(torch, mp):
-    """Achievable rates measured by the library's own probe kernels: each MFMA
+    """Achievable rates measured by the probe kernels (libmpfa_probe.so): each MFMA
     form the attention kernels use, issued back to back by 8 waves per SIMD
     (2048 workgroups, 8 independent accumulators per wave), and the HBM read
     rate of a 4 GiB buffer read once through registers or directly into LDS,
@@ -212,7 +212,7 @@ def probe_peaks(torch, mp):
         out[name.replace("GBps", "blocks")] = best_blocks
     del buf
     torch.cuda.empty_cache()
-    out["note"] = ("probe kernels of libmpfa (mpfa_probe_mfma, mpfa_probe_read): dense MFMA issue "
+    out["note"] = ("probe kernels of libmpfa_probe (mpfa_probe_mfma, mpfa_probe_read): dense MFMA issue "
                    "rate per form and single-pass HBM read rate")
     return out
 
@@ -462,6 +462,47 @@ def cpu_baseline(np, W, st, rows):
                       f"{flops:.3e} FLOP in {dt:.2f} s; quantization not timed"}
 
 
+def cpu_baseline_decode(np, W, sd):
+    """Time the CPU oracle's split-KV decode on a bounded sample of the decode
+    batch: the shortest and the median sequence, every query head, the batch's
+    partition.  The oracle quantizes those contexts itself (statistics over the
+    context, then the new token appended with them frozen), untimed; the decode
+    call is timed and its algorithmic bytes counted as for the GPU launch."""
+    from oracle import oracle as orc
+    orc.build()
+    wl = sd["wl"]
+    lens = np.asarray(sd["lens"])
+    order = np.argsort(lens)
+    picks = [int(order[0]), int(order[len(order) // 2])]
+    dt = 0.0
+    nbytes = 0
+    for b in picks:
+        kv = int(lens[b])
+        ctx = kv - 1
+        log(f"cpu baseline: oracle quantization of decode sequence {b} ({ctx} context tokens) ...")
+        q, k, v = W.gen_qkv(wl.seed, [ctx], wl.h_q, wl.h_kv, wl.outliers, "cuda", seq_ids=[b])
+        npg = (kv + 63) // 64
+        pt = np.arange(npg, dtype=np.int32).reshape(1, npg)
+        r0 = orc.quantize_qk(W.bits(q), W.bits(k), W.bits(v), np.array([0, ctx], np.int32),
+                             np.arange(ctx, dtype=np.int64), npg, orc.SMOOTH | orc.COMPUTE_STATS)
+        del q, k, v
+        qn, kn, vn = W.gen_qkv(wl.seed, [1], wl.h_q, wl.h_kv, wl.outliers, "cuda", tok_offsets=[ctx],
+                               seq_ids=[b])
+        r = orc.quantize_qk(W.bits(qn), W.bits(kn), W.bits(vn), np.array([0, 1], np.int32),
+                            np.array([ctx], np.int64), npg, orc.SMOOTH, q_mean=r0["q_mean"],
+                            k_mean=r0["k_mean"], k_tscale=r0["k_tscale"], cache=r0["cache"])
+        items = np.array([(0, h) for h in range(wl.h_q)], np.int32)
+        t0 = time.perf_counter()
+        orc.decode(r["cache"], pt, np.array([kv], np.int32), r["k_tscale"], r["q_codes"], r["q_scales"],
+                   r["q_tscale"], sd["part"], items, smooth=True)
+        dt += time.perf_counter() - t0
+        nbytes += kv * (wl.h_kv * 200 + wl.h_q * 2) + wl.h_q * (72 + 4 + 256) + npg * 4 + 4
+    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": orc.num_threads(), "kind": "oracle",
+            "sample": f"sequences {picks} of the decode batch (contexts {[int(lens[b]) for b in picks]}), "
+                      f"all {wl.h_q} query heads, partition {sd['part']}: {nbytes:.3e} algorithmic bytes "
+                      f"in {dt:.2f} s; quantization not timed"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -685,6 +726,9 @@ def main():
         decode_ms = sum(t.ms() for t in ts) / args.steps
         nbytes = decode_bytes(sd)
         gbs = nbytes / (decode_ms * 1e-3) / 1e9
+        if not args.no_cpu_baseline:
+            cpu_dec = cpu_baseline_decode(np, W, sd)
+            res.setdefault("cpu_baseline", {"kind": "oracle"})["decode"] = cpu_dec
         res["decode"] = {"ms": decode_ms, "ms_min": min(t.ms() for t in ts), "GB/s": gbs,
                          "frac_hbm": gbs * 1e9 / PEAK_HBM,
                          "bytes": nbytes, "traffic": measured_traffic("decode_kernel"),
@@ -789,7 +833,8 @@ def main():
         if "decode" in res and pk.get("copy_GBps"):
             res["decode"]["frac_of_device_copy"] = res["decode"]["GB/s"] / pk["copy_GBps"]
         log("probe kernels: MFMA issue rates and HBM read rate ...")
-        pp = probe_peaks(torch, mp)
+        from paper_2609_33135_amd import probe as probe_lib
+        pp = probe_peaks(torch, probe_lib)
         res["measured_peaks"]["probe"] = pp
         if "prefill" in res:
             # the same time weighting as the specification peaks: half the FLOP in

@@ -1,5 +1,6 @@
 /*
- * Measurement probes of libmpfa.so: the achievable matrix-core rate of each
+ * Measurement probes, built as libmpfa_probe.so for the benchmark (the product
+ * library libmpfa.so does not contain them): the achievable matrix-core rate of each
  * MFMA form the attention kernels use, and the achievable HBM read rate, both
  * measured on the device itself.  They serve as the second denominator of the
  * kernels' roofline fractions, next to the published peaks (dense MFMA: FP16

@@ -23,10 +23,7 @@ HEAD_DIM, PAGE, TILE = 128, 64, 128
 
 EXPORTED = ("mpfa_quantize_qk", "mpfa_prefill", "mpfa_decode_workspace_size",
             "mpfa_decode_choose_partition", "mpfa_decode_paged", "mpfa_mixed_workspace_size",
-            "mpfa_mixed_step", "mpfa_convert", "mpfa_status_string", "mpfa_version",
-            "mpfa_probe_mfma", "mpfa_probe_read")
-PROBE_MFMA_F16, PROBE_MFMA_FP8, PROBE_MFMA_FP4 = 0, 1, 2
-PROBE_READ_VGPR, PROBE_READ_LDS = 0, 1
+            "mpfa_mixed_step", "mpfa_convert", "mpfa_status_string", "mpfa_version")
 
 
 class MpfaError(RuntimeError):
@@ -111,11 +108,6 @@ def _load(path):
         L.mpfa_status_string.restype = C.c_char_p
         L.mpfa_status_string.argtypes = [C.c_int]
         L.mpfa_version.restype = C.c_char_p
-        L.mpfa_probe_mfma.restype = C.c_int
-        L.mpfa_probe_mfma.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_uint32, C.c_uint32, C.c_void_p,
-                                      C.c_void_p]
-        L.mpfa_probe_read.restype = C.c_int
-        L.mpfa_probe_read.argtypes = [C.c_int32, C.c_void_p, C.c_int64, C.c_int32, C.c_void_p, C.c_void_p]
         _libs[path] = L
     return _libs[path]
 
@@ -285,27 +277,3 @@ def convert(fmt: int, x, out, stream=None):
     converters the quantization pass uses; 0x100 + c: E2M1 of x / e4m3(c) by the
     NVFP4 quantizer's division; 0x200 + b: E2M1 of x / 2^(b-127) (MXFP4)."""
     _check(lib().mpfa_convert(fmt, _ptr(x), x.numel(), _ptr(out), _stream(stream)), "mpfa_convert")
-
-
-# Operand words that make every A and B element 1.0 in each probe form.
-PROBE_ONES = {PROBE_MFMA_F16: 0x3C003C00, PROBE_MFMA_FP8: 0x38383838, PROBE_MFMA_FP4: 0x22222222}
-
-
-def probe_mfma(kind: int, iters: int, blocks: int, sink, pa=None, pb=None, stream=None):
-    """mpfa_probe_mfma: `blocks` x 4 waves, each `iters` rounds of 8 MFMAs of
-    form `kind`; sink is a float32 tensor of blocks * 256 elements.  Returns the
-    FLOP count of the launch."""
-    pa = PROBE_ONES[kind] if pa is None else pa
-    pb = PROBE_ONES[kind] if pb is None else pb
-    _check(lib().mpfa_probe_mfma(kind, iters, blocks, pa, pb, _ptr(sink), _stream(stream)), "mpfa_probe_mfma")
-    k = 32 if kind == PROBE_MFMA_F16 else 128
-    return blocks * 4 * iters * 8 * (2 * 16 * 16 * k)
-
-
-def probe_read(mode: int, buf, blocks: int, sink, stream=None):
-    """mpfa_probe_read: read every byte of the device tensor `buf` once; sink is
-    an int32 tensor of blocks * 256 elements (XOR of each thread's words)."""
-    nbytes = buf.numel() * buf.element_size()
-    _check(lib().mpfa_probe_read(mode, _ptr(buf), nbytes, blocks, _ptr(sink), _stream(stream)),
-           "mpfa_probe_read")
-    return nbytes

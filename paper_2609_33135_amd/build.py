@@ -1,5 +1,6 @@
 """Build libmpfa.so (HIP kernels for gfx950 + the C ABI) and its data-checking
-twin libmpfa_debug.so in-tree with hipcc."""
+twin libmpfa_debug.so in-tree with hipcc, plus libmpfa_probe.so, the
+measurement probes the benchmark loads (not part of the product library)."""
 from __future__ import annotations
 
 import os
@@ -14,8 +15,9 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmpfa.so")
 
-SOURCES = ["api.cpp", "quantize.hip", "prefill.hip", "decode.hip", "mixed.hip", "debug_checks.hip", "probe.hip"]
+SOURCES = ["api.cpp", "quantize.hip", "prefill.hip", "decode.hip", "mixed.hip", "debug_checks.hip"]
 DEBUG_LIB = os.path.join(PKG, "libmpfa_debug.so")
+PROBE_LIB = os.path.join(PKG, "libmpfa_probe.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CLANG = os.environ.get("MPFA_CLANG", "/opt/rocm/lib/llvm/bin/clang++")
 ARCH = os.environ.get("MPFA_ARCH", "gfx950")
@@ -62,17 +64,19 @@ def _link(out: str, objs: list[str]) -> None:
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source, then link libmpfa.so and libmpfa_debug.so (the same
-    kernels; its entry points also check the data they are handed)."""
+    """Compile every source, then link libmpfa.so, libmpfa_debug.so (the same
+    kernels; its entry points also check the data they are handed) and the
+    benchmark's probe library."""
     os.makedirs(BUILD, exist_ok=True)
-    jobs = [(s, False) for s in SOURCES] + [("api.cpp", True)]
+    jobs = [(s, False) for s in SOURCES] + [("api.cpp", True), ("probe.hip", False)]
     with ThreadPoolExecutor(max_workers=len(jobs)) as ex:
         objs = list(ex.map(lambda j: _compile(*j), jobs))
     kernels = objs[1:len(SOURCES)]
     _link(LIB, [objs[0], *kernels])
-    _link(DEBUG_LIB, [objs[-1], *kernels])
+    _link(DEBUG_LIB, [objs[len(SOURCES)], *kernels])
+    _link(PROBE_LIB, [objs[len(SOURCES) + 1]])
     if verbose:
-        print("built", LIB, DEBUG_LIB)
+        print("built", LIB, DEBUG_LIB, PROBE_LIB)
     return LIB
 
 

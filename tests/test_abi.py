@@ -11,13 +11,10 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def _declared():
-    names = set()
-    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
-        text = open(h).read()
-        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-        names |= set(re.findall(r"\b(mpfa_[a-z0-9_]+)\s*\(", text))
-    return names
+def _declared(header="mpfa.h"):
+    text = open(os.path.join(ROOT, "include", header)).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return set(re.findall(r"\b(mpfa_[a-z0-9_]+)\s*\(", text))
 
 
 @pytest.fixture(scope="module")
@@ -30,13 +27,31 @@ def mp():
     return mp
 
 
+def test_headers_are_covered():
+    assert sorted(os.path.basename(h) for h in glob.glob(os.path.join(ROOT, "include", "*.h"))) == \
+        ["mpfa.h", "mpfa_probe.h"]
+
+
 def test_exports_every_declared_symbol(mp):
     names = _declared()
     assert {"mpfa_quantize_qk", "mpfa_prefill", "mpfa_decode_paged"} <= names
     L = C.CDLL(mp.LIB_PATH)
     for n in sorted(names):
-        assert hasattr(L, n), f"{n} declared in include/ but not exported"
+        assert hasattr(L, n), f"{n} declared in include/mpfa.h but not exported"
     assert set(mp.EXPORTED) == names
+
+
+def test_probe_library_is_separate(mp):
+    """The measurement probes live in the benchmark's libmpfa_probe.so, which
+    exports what include/mpfa_probe.h declares; the product library has none."""
+    from paper_2609_33135_amd import probe
+    names = _declared("mpfa_probe.h")
+    assert set(probe.EXPORTED) == names
+    P = C.CDLL(probe.PROBE_LIB_PATH)
+    L = C.CDLL(mp.LIB_PATH)
+    for n in sorted(names):
+        assert hasattr(P, n), f"{n} missing from libmpfa_probe.so"
+        assert not hasattr(L, n), f"{n} still exported by the product library"
 
 
 def test_debug_library_exports_the_same_symbols(mp):
@@ -173,7 +188,8 @@ def test_mixed_step_validation(mp):
 def test_probe_validation(mp):
     """The measurement probes reject bad arguments on the host; the fake device
     addresses below are never dereferenced."""
-    L = mp.lib()
+    from paper_2609_33135_amd import probe
+    L = probe.lib()
     sink = 0x1000
     for kind, iters, blocks, s in ((3, 1, 1, sink), (-1, 1, 1, sink), (0, 0, 1, sink), (0, 1, 0, sink),
                                    (0, 1, (1 << 20) + 1, sink), (0, 1, 1, None)):

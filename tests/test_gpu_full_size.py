@@ -7,6 +7,8 @@ sampled outputs one by one:
     quantizer output compared bit for bit, sampled rows of several heads;
   * Llama-3.1-8B-shaped paged decode, batch 32, contexts U[16384, 131072]:
     every query head of the shortest, the longest and one middle sequence;
+  * the same decode with all 32 contexts at 131072 keys (partition 4096);
+  * the MXFP4 variant of the 131072-token prefill;
   * the mixed serving step (Qwen shapes): a 32768-token chunk at position
     65536 over its paged prefix, plus 64 decode sequences, one launch sequence
     on one stream; sampled chunk rows and sampled decode sequences.
@@ -134,6 +136,54 @@ def test_llama_decode_batch32(orc, mp, bench, W):
         o16 = _oracle_decode_one(orc, W, wl.seed, b, int(lens[b]), wl.h_q, wl.h_kv, wl.outliers,
                                  sd["part"])
         _report(f"llama decode seq {b} kv {lens[b]} partition {sd['part']}", out[b], o16)
+
+
+def test_llama_decode_128k_partition4096(orc, mp, bench, W):
+    """The decode_128k point of the benchmark: 32 contexts of 131072 keys, the
+    partition the benchmark's policy picks (4096 tokens); the first, a middle
+    and the last sequence, every query head."""
+    print("case: llama decode 32 x 131072 (bench launch)", flush=True)
+    sd = bench.setup_decode(torch, np, mp, W, 32, ctx_range=(131072, 131072))
+    assert sd["part"] == 4096, sd["part"]
+    bench.run_decode(mp, sd)
+    torch.cuda.synchronize()
+    out = H.bits(sd["out"])
+    wl = sd["wl"]
+    lens = np.asarray(sd["lens"])
+    for b in (0, 15, 31):
+        o16 = _oracle_decode_one(orc, W, wl.seed, b, int(lens[b]), wl.h_q, wl.h_kv, wl.outliers,
+                                 sd["part"])
+        _report(f"llama decode 128k seq {b} partition {sd['part']}", out[b], o16)
+
+
+def test_qwen_prefill_131072_mxfp4(orc, mp, bench, W):
+    """The MXFP4 variant at the full Qwen size in the benchmark's launch: every
+    code and E8M0 scale bit for bit, sampled rows of four heads."""
+    seq = 131072
+    print(f"case: qwen prefill {seq} mxfp4 full-size (bench launch)", flush=True)
+    st = bench.setup_prefill(torch, np, mp, W, seq, smooth=True, mx=True)
+    bench.run_quant(mp, st)
+    bench.run_prefill(mp, st)
+    torch.cuda.synchronize()
+    out = H.bits(st["out"])
+    ref = orc.quantize_qk(H.bits(st["q"]), H.bits(st["k"]), H.bits(st["v"]),
+                          np.array([0, seq], np.int32), W.slots_for(st["pt"], 0, range(seq)),
+                          st["n_pages"], orc.SMOOTH | orc.COMPUTE_STATS | orc.MXFP4)
+    print("oracle quantization done", flush=True)
+    assert np.array_equal(st["qq"].codes.cpu().numpy(), ref["q_codes"])
+    assert np.array_equal(st["qq"].scales.cpu().numpy(), ref["q_scales"])
+    rc = ref["cache"]
+    for name in ("k_codes", "k_scales", "v_codes"):
+        assert np.array_equal(getattr(st["cache"], name).cpu().numpy(), rc[name]), name
+    assert np.array_equal(H.bits(st["cache"].ds), rc["ds"])
+    rng = np.random.default_rng(4)
+    rows = np.unique(np.concatenate([np.arange(0, 130, 9), rng.integers(0, seq, 20),
+                                     np.arange(seq - 130, seq, 13), [seq - 1]]))
+    heads = [0, 9, 26, 39]
+    items = np.array([(0, int(r), h) for r in rows for h in heads], np.int32)
+    o16, _ = orc.prefill(rc, st["pt"], [seq], ref["k_tscale"], ref["q_codes"], ref["q_scales"],
+                         ref["q_tscale"], [0, seq], [0], items, mxfp4=True)
+    _report(f"qwen prefill {seq} mxfp4", out[items[:, 1], items[:, 2]], o16)
 
 
 def test_mixed_step_qwen(orc, mp, W):

@@ -11,7 +11,7 @@ pytestmark = pytest.mark.gpu
 @pytest.fixture(scope="module")
 def mp():
     import torch
-    import paper_2609_33135_amd as mp
+    from paper_2609_33135_amd import probe as mp
     assert torch.cuda.is_available()
     mp.lib()
     return mp
