@@ -281,6 +281,28 @@ mpfa_status mpfa_decode_choose_partition(int32_t batch, const int32_t* kv_len_ho
 mpfa_status mpfa_decode_paged(const mpfa_decode_args* args, void* workspace, size_t workspace_bytes,
                               mpfa_stream_t stream);
 
+/* Size of the library's own decode scratch on each GPU (partition states of
+ * mpfa_decode_paged_static). */
+#define MPFA_STATIC_SCRATCH_BYTES (64u << 20)
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * mpfa_decode_paged without the workspace argument.  The same kernels keep
+ * their partition states in a device array of MPFA_STATIC_SCRATCH_BYTES that
+ * the library holds on each GPU it runs on until the process ends; the caller
+ * still passes the inputs and the output.  The call allocates nothing: its
+ * first call on a device only looks up that device's address of the array.
+ * Arguments, layouts and results are exactly those of mpfa_decode_paged.
+ * Errors: as mpfa_decode_paged, and MPFA_ERR_WORKSPACE, before any launch,
+ * when mpfa_decode_workspace_size(batch, h_q, max_partitions) exceeds
+ * MPFA_STATIC_SCRATCH_BYTES.  Every call on a GPU shares that GPU's array:
+ * calls that overlap on one GPU (concurrent streams, or threads) race and
+ * must be serialized by the caller; the array keeps the last call's states,
+ * and no call needs it to start at any particular value.
+ */
+mpfa_status mpfa_decode_paged_static(const mpfa_decode_args* args, mpfa_stream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* Mixed serving step in one launch (Sec. 7.3; prefill and decode requests    */
 /* of one step served together)                                               */

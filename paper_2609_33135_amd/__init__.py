@@ -20,9 +20,11 @@ LIB_PATH = DEBUG_LIB_PATH if os.environ.get("MPFA_DEBUG") == "1" else os.path.jo
 SMOOTH, COMPUTE_STATS, TSCALE_UNIT, SEED_MFMA, MXFP4, SEED_ELEMWISE = 1, 2, 4, 8, 16, 32
 PV_BF16, PV_NVFP4 = 64, 128
 HEAD_DIM, PAGE, TILE = 128, 64, 128
+STATIC_SCRATCH_BYTES = 64 << 20   # MPFA_STATIC_SCRATCH_BYTES
 
 EXPORTED = ("mpfa_quantize_qk", "mpfa_prefill", "mpfa_decode_workspace_size",
-            "mpfa_decode_choose_partition", "mpfa_decode_paged", "mpfa_mixed_workspace_size",
+            "mpfa_decode_choose_partition", "mpfa_decode_paged", "mpfa_decode_paged_static",
+            "mpfa_mixed_workspace_size",
             "mpfa_mixed_step", "mpfa_convert", "mpfa_status_string", "mpfa_version")
 
 
@@ -97,6 +99,8 @@ def _load(path):
                                                    C.POINTER(C.c_int32)]
         L.mpfa_decode_paged.restype = C.c_int
         L.mpfa_decode_paged.argtypes = [C.POINTER(DecodeArgs), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.mpfa_decode_paged_static.restype = C.c_int
+        L.mpfa_decode_paged_static.argtypes = [C.POINTER(DecodeArgs), C.c_void_p]
         L.mpfa_mixed_workspace_size.restype = C.c_int
         L.mpfa_mixed_workspace_size.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                                 C.POINTER(C.c_size_t)]
@@ -234,6 +238,26 @@ def decode_paged(qq: QuantQ, cache: PagedCache, stats: SeqStats, kv_len, page_ta
     _check(lib().mpfa_decode_paged(C.byref(a), _ptr(workspace),
                                    workspace.numel() * workspace.element_size(), _stream(stream)),
            "mpfa_decode_paged")
+
+
+def _decode_args(qq, cache, stats, kv_len, page_table, out, partition_tokens, max_partitions, flags):
+    return DecodeArgs(batch=kv_len.numel(), h_q=qq.codes.shape[1], h_kv=cache.h_kv,
+                      head_dim=HEAD_DIM, max_pages=page_table.shape[1],
+                      partition_tokens=partition_tokens, max_partitions=max_partitions, flags=flags,
+                      kv_len=_ptr(kv_len), page_table=_ptr(page_table), q_codes=_ptr(qq.codes),
+                      q_scales=_ptr(qq.scales), q_tscale=_ptr(qq.tscale),
+                      k_codes=_ptr(cache.k_codes), k_scales=_ptr(cache.k_scales),
+                      v_codes=_ptr(cache.v_codes), ds=_ptr(cache.ds),
+                      k_tscale=_ptr(stats.k_tscale), out=_ptr(out), num_pages=cache.num_pages)
+
+
+def decode_paged_static(qq: QuantQ, cache: PagedCache, stats: SeqStats, kv_len, page_table, out,
+                        partition_tokens: int, max_partitions: int, flags: int, stream=None):
+    """mpfa_decode_paged_static: decode_paged with the partition states in the
+    library's per-GPU scratch array instead of a caller workspace (for callers
+    that cannot allocate; calls on one GPU must not overlap)."""
+    a = _decode_args(qq, cache, stats, kv_len, page_table, out, partition_tokens, max_partitions, flags)
+    _check(lib().mpfa_decode_paged_static(C.byref(a), _stream(stream)), "mpfa_decode_paged_static")
 
 
 def mixed_workspace_size(batch: int, h_q: int, h_kv: int, max_partitions: int) -> int:

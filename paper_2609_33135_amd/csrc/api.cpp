@@ -10,6 +10,9 @@
 
 #include "mpfa_internal.h"
 
+static_assert(MPFA_STATIC_SCRATCH_BYTES == mpfa::kStaticScratchBytes,
+              "public and internal sizes of the static decode scratch must agree");
+
 #ifdef MPFA_DEBUG_CHECKS
 #include <vector>
 #endif
@@ -169,9 +172,9 @@ static mpfa_status prefill_params(const mpfa_prefill_args* a, mpfa::PrefillParam
 }
 
 
-// Host-side validation of the decode arguments and their launch parameters.
-static mpfa_status decode_params(const mpfa_decode_args* a, void* workspace, size_t workspace_bytes,
-                                 mpfa::DecodeParams& p) {
+// Host-side validation of the decode arguments and their launch parameters,
+// apart from the workspace.
+static mpfa_status decode_args_params(const mpfa_decode_args* a, mpfa::DecodeParams& p) {
   if (!a) return MPFA_ERR_INVALID;
   if (a->head_dim != MPFA_HEAD_DIM) return a->head_dim > 0 ? MPFA_ERR_UNSUPPORTED : MPFA_ERR_INVALID;
   if (a->batch < 1 || a->batch > 65535 || a->max_pages < 1 || a->max_partitions < 1)
@@ -199,7 +202,6 @@ static mpfa_status decode_params(const mpfa_decode_args* a, void* workspace, siz
   size_t need = 0;
   if (mpfa_decode_workspace_size(a->batch, a->h_q, a->max_partitions, &need) != MPFA_OK)
     return MPFA_ERR_INVALID;
-  if (!workspace || workspace_bytes < need) return MPFA_ERR_WORKSPACE;
 
   p = mpfa::DecodeParams{};
   p.batch = a->batch;
@@ -221,8 +223,20 @@ static mpfa_status decode_params(const mpfa_decode_args* a, void* workspace, siz
   p.v_codes = a->v_codes;
   p.ds = static_cast<const uint16_t*>(a->ds);
   p.k_tscale = a->k_tscale;
-  p.ws = static_cast<float*>(workspace);
+  p.ws = nullptr;
   p.out = static_cast<uint16_t*>(a->out);
+  return MPFA_OK;
+}
+
+// Decode arguments plus a caller-provided workspace of workspace_bytes.
+static mpfa_status decode_params(const mpfa_decode_args* a, void* workspace, size_t workspace_bytes,
+                                 mpfa::DecodeParams& p) {
+  const mpfa_status st = decode_args_params(a, p);
+  if (st != MPFA_OK) return st;
+  size_t need = 0;
+  mpfa_decode_workspace_size(a->batch, a->h_q, a->max_partitions, &need);
+  if (!workspace || workspace_bytes < need) return MPFA_ERR_WORKSPACE;
+  p.ws = static_cast<float*>(workspace);
   return MPFA_OK;
 }
 
@@ -347,6 +361,24 @@ mpfa_status mpfa_decode_paged(const mpfa_decode_args* a, void* workspace, size_t
   st = check_decode(a, reinterpret_cast<hipStream_t>(stream));
   if (st != MPFA_OK) return st;
 #endif
+  return mpfa::launch_decode(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
+                                                                                      : MPFA_ERR_HIP;
+}
+
+mpfa_status mpfa_decode_paged_static(const mpfa_decode_args* a, mpfa_stream_t stream) {
+  mpfa::DecodeParams p;
+  mpfa_status st = decode_args_params(a, p);
+  if (st != MPFA_OK) return st;
+  size_t need = 0;
+  mpfa_decode_workspace_size(a->batch, a->h_q, a->max_partitions, &need);
+  if (need > MPFA_STATIC_SCRATCH_BYTES) return MPFA_ERR_WORKSPACE;
+#ifdef MPFA_DEBUG_CHECKS
+  st = check_decode(a, reinterpret_cast<hipStream_t>(stream));
+  if (st != MPFA_OK) return st;
+#endif
+  void* ws = nullptr;
+  if (mpfa::static_decode_scratch(&ws) != hipSuccess) return MPFA_ERR_HIP;
+  p.ws = static_cast<float*>(ws);
   return mpfa::launch_decode(p, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? MPFA_OK
                                                                                       : MPFA_ERR_HIP;
 }

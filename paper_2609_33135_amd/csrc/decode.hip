@@ -15,7 +15,37 @@
 // every lane's code bytes are contiguous; Q uses the same permutation.
 #include "decode_body.h"
 
+#include <mutex>
+
 namespace mpfa {
+
+// Partition states of mpfa_decode_paged_static: one array per GPU, created
+// with the code object and held until the process ends.  Host code never uses
+// the name itself (on the host it only stands for the symbol); it uses the
+// device address that hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_addr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t static_decode_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_addr[dev]) {
+    void* a = nullptr;
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    scratch_addr[dev] = a;
+  }
+  *ptr = scratch_addr[dev];
+  return hipSuccess;
+}
 
 namespace {
 

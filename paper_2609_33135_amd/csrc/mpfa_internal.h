@@ -12,6 +12,9 @@ constexpr int kMaxKvHeadsQuant = 32;
 // map (each workgroup looks its work up with an O(batch) scan); larger ones a
 // three-dimensional grid
 constexpr int kDecodePackedMaxBatch = 512;
+// size of the per-GPU device array that holds the decode partition states of
+// mpfa_decode_paged_static (the entry point for callers that cannot allocate)
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
 
 struct QuantParams {
   int batch, total_tokens, max_seqlen, h_q, h_kv;
@@ -103,5 +106,8 @@ hipError_t launch_mixed(const MixedParams& m, hipStream_t stream);
 hipError_t launch_convert(int fmt, const float* x, int64_t n, uint8_t* out, hipStream_t stream);
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams& p, hipStream_t stream);
+// Device address of the static decode scratch array on the current device
+// (looked up once per device, then cached).
+hipError_t static_decode_scratch(void** ptr);
 
 }  // namespace mpfa

@@ -127,6 +127,23 @@ def test_decode_workspace_checks(mp):
     assert mp.lib().mpfa_decode_paged(C.byref(a), 0x1000, need - 1, None) == 3
 
 
+def test_decode_static_validation(mp):
+    """The allocation-free decode rejects bad arguments like mpfa_decode_paged,
+    and states larger than the static scratch with MPFA_ERR_WORKSPACE, all on
+    the host before any HIP call (this runs without a GPU)."""
+    L = mp.lib()
+    for field, value, status in (("partition_tokens", 100, 1), ("h_q", 72, 2), ("kv_len", None, 1)):
+        a = _decode_args(mp, **{field: value})
+        assert L.mpfa_decode_paged_static(C.byref(a), None) == status
+    limit = mp.STATIC_SCRATCH_BYTES
+    per_partition = 32 * 130 * 4                 # one partition state of every query head
+    fits = limit // (2 * per_partition)          # batch 2
+    assert mp.decode_workspace_size(2, 32, fits) <= limit < mp.decode_workspace_size(2, 32, fits + 1)
+    a = _decode_args(mp, max_partitions=fits + 1)
+    assert L.mpfa_decode_paged_static(C.byref(a), None) == mp.MPFA_ERR_WORKSPACE
+    assert mp.debug_lib().mpfa_decode_paged_static(C.byref(a), None) == mp.MPFA_ERR_WORKSPACE
+
+
 def test_choose_partition(mp):
     lens = np.array([16384, 131072, 50000, 8000] * 8, np.int32)
     p = mp.decode_choose_partition(lens, 8, 256)
