@@ -70,13 +70,11 @@ __device__ __forceinline__ int partition_groups(int kvl, int partition_tokens) {
 
 template <bool SMOOTH, bool MX, bool PACKED>
 __global__ __launch_bounds__(kWavesPerBlock * 64, 2) void decode_kernel(DecodeParams p) {
-  __shared__ __attribute__((aligned(16))) uint8_t vlds[kWavesPerBlock * kVBytes];
   const int wave = threadIdx.x >> 6;
   if (!PACKED) {
     // grid (partition group, KV head, sequence); groups past the sequence's
     // partitions return inside decode_partition
-    decode_partition<SMOOTH, MX, false>(p, blockIdx.z, blockIdx.y, blockIdx.x * kWavesPerBlock + wave,
-                                        vlds + wave * kVBytes, nullptr);
+    decode_partition<SMOOTH, MX, false>(p, blockIdx.z, blockIdx.y, blockIdx.x * kWavesPerBlock + wave, nullptr);
     return;
   }
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
@@ -104,14 +102,16 @@ __global__ __launch_bounds__(kWavesPerBlock * 64, 2) void decode_kernel(DecodePa
     base += total;
   }
   if (b < 0) return;   // the grid is sized for batch * ceil(max_partitions / 4) pairs
-  decode_partition<SMOOTH, MX, false>(p, b, hk, grp * kWavesPerBlock + wave, vlds + wave * kVBytes, nullptr);
+  decode_partition<SMOOTH, MX, false>(p, b, hk, grp * kWavesPerBlock + wave, nullptr);
 }
 
-// One workgroup (128 threads, one per channel) per (sequence, query head).
-__global__ __launch_bounds__(128) void merge_kernel(DecodeParams p) {
-  const int h = blockIdx.x, b = blockIdx.y, d = threadIdx.x;
-  const int np = (p.kv_len[b] + p.partition_tokens - 1) / p.partition_tokens;
-  p.out[((int64_t)b * p.h_q + h) * kD + d] = bf16_rne(merge_channel(p, b, h, d, np));
+// One wave per (sequence, query head).  A separate launch: merging in the
+// last-arriving decode wave needs the partition states made visible across
+// the XCDs' L2 caches (an L2 write-back per wave, or write-through stores and
+// an arrival counter), which measured slower than this second launch.
+__global__ __launch_bounds__(64) void merge_kernel(DecodeParams p) {
+  const int h = blockIdx.x, b = blockIdx.y;
+  merge_head(p, b, h, (p.kv_len[b] + p.partition_tokens - 1) / p.partition_tokens);
 }
 
 }  // namespace
@@ -142,7 +142,7 @@ hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  merge_kernel<<<dim3(p.h_q, p.batch), dim3(128), 0, stream>>>(p);
+  merge_kernel<<<dim3(p.h_q, p.batch), dim3(64), 0, stream>>>(p);
   return hipGetLastError();
 }
 

@@ -10,27 +10,23 @@ namespace mpfa {
 namespace {
 
 constexpr int kWavesPerBlock = 4;
-constexpr int kVBytes = kD * kTile;   // one FP8 V tile per wave in LDS (16 KB)
 
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-typedef __attribute__((address_space(1))) void* global_ptr_t;
+// Per wave, tile j (last to first): PV of tile j+1 (V and P in registers);
+// loads of V tile j; QK of tile j (K codes prefetched in registers); loads of
+// tile j-1's K codes, scales and compensation; online softmax of tile j.  The
+// V loads land directly in the PV operand registers: lane l holds channel
+// 16 db + l%16, keys 32 (l/16) + 16 hf .. +15 in va[db] (hf 0) and vb[db]
+// (hf 1).  Every load goes to registers (none to LDS), so the compiler counts
+// each wait: PV of tile j+1 waits for V(j+1) with K(j) still in flight, QK of
+// tile j for K(j) with V(j) in flight.
 
-// Software pipeline per wave, iteration j (tiles last to first):
-//   wait for every outstanding load;  PV of tile j+1 (V from LDS, P from
-//   registers);  direct global->LDS loads of V tile j;  QK of tile j (K codes
-//   prefetched in registers);  prefetch of tile j-1's K codes, scales and
-//   compensation;  online softmax of tile j.
-// V never occupies registers (it is read from LDS as MFMA operands), which
-// keeps the wave under the register budget of two waves per SIMD.
-// LDS V layout: for channel block db and half hf, the 1 KB slab at
-// (2 db + hf) KB holds, at 16 * lane, the bytes the lane feeds to the MFMA:
-// channel 16 db + lane%16, keys 32 (lane/16) + 16 hf .. +15.
-// Merge of the partition states of one (sequence, query head) for output
-// channel d: log-sum-exp over the partitions in order, then O / L, BF16.
-// The loads of 16 partitions are issued together; the accumulation order stays
-// partition 0, 1, 2, ...
-__device__ __forceinline__ float merge_channel(const DecodeParams& p, int b, int h, int d, int np) {
+// Merge of the partition states of query head h of sequence b by one wave:
+// lane l owns channels l and l + 64.  Per channel: the maximum of m over the
+// partitions, then L and O accumulated over the partitions in order, O / L
+// rounded to BF16.  The loads of 16 partitions are issued together.
+__device__ __forceinline__ void merge_head(const DecodeParams& p, int b, int h, int np) {
   constexpr int kBatch = 16;
+  const int lane = threadIdx.x & 63;
   const float* st = p.ws + ((int64_t)b * p.h_q + h) * p.max_partitions * (kD + 2);
   float M = -INFINITY;
   for (int q0 = 0; q0 < np; q0 += kBatch) {
@@ -40,38 +36,46 @@ __device__ __forceinline__ float merge_channel(const DecodeParams& p, int b, int
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) M = fmaxf(M, mv[j]);
   }
-  float L = 0.0f, O = 0.0f;
+  float L = 0.0f, O0 = 0.0f, O1 = 0.0f;
   for (int q0 = 0; q0 < np; q0 += kBatch) {
-    float mv[kBatch], lv[kBatch], ov[kBatch];
+    float mv[kBatch], lv[kBatch], o0[kBatch], o1[kBatch];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       const bool in = q0 + j < np;
       const float* sq = st + (q0 + j) * (kD + 2);
       mv[j] = in ? sq[0] : 0.0f;
       lv[j] = in ? sq[1] : 0.0f;
-      ov[j] = in ? sq[2 + d] : 0.0f;
+      o0[j] = in ? sq[2 + lane] : 0.0f;
+      o1[j] = in ? sq[2 + 64 + lane] : 0.0f;
     }
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       if (q0 + j < np) {
         const float f = __builtin_amdgcn_exp2f(mv[j] - M);
         L = __builtin_fmaf(f, lv[j], L);
-        O = __builtin_fmaf(f, ov[j], O);
+        O0 = __builtin_fmaf(f, o0[j], O0);
+        O1 = __builtin_fmaf(f, o1[j], O1);
       }
     }
   }
-  return np > 0 ? __fdiv_rn(O, L) : 0.0f;
+  uint16_t* o = p.out + ((int64_t)b * p.h_q + h) * kD;
+  o[lane] = bf16_rne(np > 0 ? __fdiv_rn(O0, L) : 0.0f);
+  o[64 + lane] = bf16_rne(np > 0 ? __fdiv_rn(O1, L) : 0.0f);
 }
 
 // One decode work item (sequence b, KV head hk, partition part) executed by
-// one wave with the 16 KB LDS slab vbuf.  With FUSED, the wave that completes
-// the last partition of (b, hk) also merges the group's query heads: each wave
-// publishes its state, then counts itself in counters[b * h_kv + hk] (device
-// scope); the last arrival reads all states, writes the outputs and resets the
-// counter to zero for the next call.
+// one wave; it writes the partition state to the workspace.  With FUSED, the
+// wave then counts itself in counters[b * h_kv + hk] (device scope); the wave
+// that completes the last partition of (b, hk) merges the group's query heads,
+// writes the outputs and resets the counter to zero for the next call.
 template <bool SMOOTH, bool MX, bool FUSED>
-__device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, int hk, int part, uint8_t* vbuf,
+__device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, int hk, int part,
                                                  uint32_t* counters) {
+  // the item indices are wave-uniform: in scalar registers, the tile loop and
+  // its branches are scalar too
+  b = __builtin_amdgcn_readfirstlane(b);
+  hk = __builtin_amdgcn_readfirstlane(hk);
+  part = __builtin_amdgcn_readfirstlane(part);
   const int lane = threadIdx.x & 63, g = lane >> 4, lr = lane & 15;
   const int kvl = p.kv_len[b];
   const int np = (kvl + p.partition_tokens - 1) / p.partition_tokens;
@@ -111,6 +115,7 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
     }
   }
 
+  const int j_lo_ = kbeg / kTile, j_hi_ = (kend - 1) / kTile;
   const int krow_in_tile = 32 * (lr >> 2) + (lr & 3);   // + 4 mb: key of MFMA row lr
   const int64_t page_k_rows = (int64_t)p.h_kv * kPage;   // K rows per page
   const int64_t kv_head = (int64_t)hk * kPage;
@@ -122,42 +127,61 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
   u32x4 kc[8];
   uint32_t ksc[8];
   uint2 dsw[8];
-  // The pages of tile j that the lane reads: its K rows' page (MFMA rows 0..7
-  // hold keys 0..63) and its V / Delta_S page (lane groups 0, 1: keys 0..63).
-  // They are loaded one tile ahead of their use, so no address computation
-  // waits on a page-table load (a dependent load would drain every load the
-  // wave has in flight); as per-lane values they stay in vector registers.
-  auto tile_pages = [&](int j, int& kp, int& vp) {
-    kp = pt[min(2 * j + (lr >> 3), npg - 1)];
-    vp = pt[min(2 * j + (g >> 1), npg - 1)];
+  // Page indices: 64 consecutive entries of the page table in one register
+  // (lane i holds entry base + i), read per tile with v_readlane into scalar
+  // registers.  The tile loop then issues no page-table loads, whose results
+  // (needed by the next addresses and retiring after every K and V load issued
+  // before them) would drain the loads in flight.  The window is loaded below
+  // the current pages, so a partition of up to 4096 tokens needs one load.
+  int win = 0, win_base = 0;
+  auto load_window = [&](int lo, int hi) {   // pages lo .. hi (even lo)
+    win_base = max(lo, hi - 63) & ~1;
+    win = pt[min(win_base + lane, npg - 1)];
   };
-  auto load_k = [&](int64_t kpage, int64_t dpage) {
-#pragma unroll
-    for (int mb = 0; mb < 8; ++mb) {
-      const int64_t row = kpage * page_k_rows + kv_head + ((krow_in_tile + 4 * mb) & 63);
-      kc[mb] = *reinterpret_cast<const u32x4*>(p.k_codes + row * 64 + 16 * g);
-      ksc[mb] = MX ? (uint32_t)p.k_scales[row * 8 + g]
-                   : (uint32_t)*reinterpret_cast<const uint16_t*>(p.k_scales + row * 8 + 2 * g);
+  // The two pages of tile j: keys 0..63 and 64..127.  A lane's K rows lie in
+  // page lr / 8 of the tile (MFMA rows 0..7 hold keys 0..63), its V and
+  // Delta_S bytes in page g / 2.
+  auto tile_pages = [&](int j, int& q0, int& q1) {
+    if (2 * j < win_base) {   // next window (partitions above 4096 tokens)
+      load_window(2 * j_lo_, 2 * j + 1);
+      __builtin_amdgcn_s_waitcnt(0);   // here, so the common path holds no pending window load
     }
-    // compensation of the lane's accumulator rows: keys 32g + 4mb .. +3, head lr
+    q0 = __builtin_amdgcn_readlane(win, 2 * j - win_base);
+    q1 = __builtin_amdgcn_readlane(win, 2 * j + 1 - win_base);
+  };
+  // With live false (past the partition's first tile) every lane reads row 0
+  // of its page instead: the loads stay unconditional, so they can issue
+  // between the QK products that free their registers, and cost one cache line.
+  auto load_k = [&](int64_t kpage, int64_t dpage, bool live) {
+    const int rmask = live ? 63 : 0;
+    // compensation of the lane's accumulator rows: keys 32g + 4mb .. +3, head
+    // lr; issued first, as the first QK product starts from it
     if (SMOOTH) {
-      const uint16_t* dsp = p.ds + (dpage * p.h_q + h) * kPage + ((32 * g) & 63);
+      const uint16_t* dsp = p.ds + (dpage * p.h_q + h) * kPage + ((32 * g) & rmask);
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) dsw[mb] = *reinterpret_cast<const uint2*>(dsp + 4 * mb);
     } else {
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) dsw[mb] = make_uint2(0u, 0u);
     }
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+      const int64_t row = kpage * page_k_rows + kv_head + ((krow_in_tile + 4 * mb) & rmask);
+      ksc[mb] = MX ? (uint32_t)p.k_scales[row * 8 + g]
+                   : (uint32_t)*reinterpret_cast<const uint16_t*>(p.k_scales + row * 8 + 2 * g);
+      kc[mb] = *reinterpret_cast<const u32x4*>(p.k_codes + row * 64 + 16 * g);
+    }
   };
-  // ---- V tile j: 16 direct global->LDS loads of 16 bytes per lane
+  // ---- V tile j: 16 loads of 16 bytes per lane, straight into the PV
+  // operand registers (channel 16 db + lr, keys 32 g + 16 hf .. +15)
+  u32x4 va[8], vb[8];
   auto load_v = [&](int64_t vpage) {
     const uint8_t* vsrc = p.v_codes + ((vpage * p.h_kv + hk) * kD + lr) * kPage + ((32 * g) & 63);
 #pragma unroll
-    for (int db = 0; db < 8; ++db)
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf)
-        __builtin_amdgcn_global_load_lds((global_ptr_t)(vsrc + db * 16 * kPage + 16 * hf),
-                                         (lds_ptr_t)(vbuf + (2 * db + hf) * 1024), 16, 0, 0);
+    for (int db = 0; db < 8; ++db) {
+      va[db] = *reinterpret_cast<const u32x4*>(vsrc + db * 16 * kPage);
+      vb[db] = *reinterpret_cast<const u32x4*>(vsrc + db * 16 * kPage + 16);
+    }
   };
 
   float m = -INFINITY, l = 0.0f;
@@ -165,20 +189,13 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
 #pragma unroll
   for (int db = 0; db < 8; ++db) o[db] = (f32x4){0.f, 0.f, 0.f, 0.f};
   i32x8 pb = {};
-  int pv_tile = -1;      // tile whose P (pb) awaits its PV product
 
-  // O^T += V^T P^T for tile pv_tile.  Keys past the end of the sequence carry
-  // P = 0, but their V bytes may be stale cache contents: they are cleared so
-  // that 0 * NaN cannot occur.
-  auto pv = [&]() {
-    u32x4 va[8], vb[8];
-#pragma unroll
-    for (int db = 0; db < 8; ++db) {
-      va[db] = *reinterpret_cast<const u32x4*>(vbuf + (2 * db) * 1024 + 16 * lane);
-      vb[db] = *reinterpret_cast<const u32x4*>(vbuf + (2 * db + 1) * 1024 + 16 * lane);
-    }
-    if (pv_tile * kTile + kTile > kend) {   // uniform: the partition's last keys
-      const int nv = kend - (pv_tile * kTile + 32 * g);
+  // O^T += V^T P^T for tile t (P in pb, V in the LDS slab).  Keys past the end
+  // of the sequence carry P = 0, but their V bytes may be stale cache contents:
+  // they are cleared so that 0 * NaN cannot occur.
+  auto pv = [&](int t) {
+    if (t * kTile + kTile > kend) {   // uniform: the partition's last keys
+      const int nv = kend - (t * kTile + 32 * g);
       uint32_t ma[4], mb2[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -202,18 +219,19 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
     }
   };
 
-  const int j_lo = kbeg / kTile, j_hi = (kend - 1) / kTile;
-  int cur_k, cur_v, nxt_k = 0, nxt_v = 0;   // the lane's pages of tile j, of tile j - 1
-  tile_pages(j_hi, cur_k, cur_v);
-  load_k(cur_k, cur_v);
-  tile_pages(max(j_hi - 1, j_lo), nxt_k, nxt_v);
+  const int j_lo = j_lo_, j_hi = j_hi_;
+  int c0, c1, n0, n1;   // pages of tile j, of tile j - 1
+  load_window(2 * j_lo, 2 * j_hi + 1);
+  tile_pages(j_hi, c0, c1);
+  load_k((lr >> 3) ? c1 : c0, (g >> 1) ? c1 : c0, true);
+  tile_pages(max(j_hi - 1, j_lo), n0, n1);
   for (int j = j_hi; j >= j_lo; --j) {
     const int key0 = j * kTile;
-    __builtin_amdgcn_s_waitcnt(0);   // K(j) in registers, V(j+1) in LDS
-    if (pv_tile >= 0) pv();
-    // the LDS reads of PV(j+1) must be complete before V(j) overwrites them
-    __builtin_amdgcn_s_waitcnt(0);
-    load_v(cur_v);
+    if (j < j_hi) pv(j + 1);
+    load_v((g >> 1) ? c1 : c0);
+    // V(j) is issued before the QK waits for K(j): those waits then leave the
+    // V loads in flight
+    __builtin_amdgcn_sched_barrier(0);
     // ---- S^T = 1 Delta_S^T + K Q^T (the rank-G term as accumulator input)
     f32x4 s[8];
 #pragma unroll
@@ -231,12 +249,10 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
         s[mb] = mfma_f16(dequant8(kc[mb][3], s1), qop[3], c);
       }
     }
-    if (j > j_lo) load_k(nxt_k, nxt_v);
-    // outside the branch: copying a page index inside it would make the
-    // compiler wait for the K loads at the join
-    cur_k = nxt_k;
-    cur_v = nxt_v;
-    tile_pages(max(j - 2, j_lo), nxt_k, nxt_v);
+    load_k((lr >> 3) ? n1 : n0, (g >> 1) ? n1 : n0, j > j_lo);
+    c0 = n0;
+    c1 = n1;
+    tile_pages(max(j - 2, j_lo), n0, n1);
     if (key0 + kTile > kend) {
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb)
@@ -274,10 +290,8 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
 #pragma unroll
       for (int db = 0; db < 8; ++db) o[db] *= alpha;
     }
-    pv_tile = j;
   }
-  __builtin_amdgcn_s_waitcnt(0);
-  pv();
+  pv(j_lo);
   // The scaled FP8 MFMA may otherwise be sunk into the branch below, where
   // lanes of the invalid query-head columns are switched off; the MFMA then
   // reads their (inactive) operand rows as zero.  An empty asm that consumes
@@ -299,20 +313,14 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& p, int b, i
       for (int i = 0; i < 4; ++i) st[2 + 16 * db + 4 * g + i] = o[db][i];
   }
   if (FUSED) {
-    __threadfence();   // this partition's state is visible device-wide before it is counted
+    // release: this partition's state is visible device-wide before it is counted
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     uint32_t prev = 0;
     if (lane == 0) prev = atomicAdd(&counters[b * p.h_kv + hk], 1u);
     prev = __shfl(prev, 0);
     if (prev == (uint32_t)(np - 1)) {   // last partition of (b, hk): merge its query heads
-      __threadfence();
-      for (int j = 0; j < grp; ++j) {
-        const int hq = hk * grp + j;
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const int d = lane + 64 * c;
-          p.out[((int64_t)b * p.h_q + hq) * kD + d] = bf16_rne(merge_channel(p, b, hq, d, np));
-        }
-      }
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");   // every state counted before is visible
+      for (int j = 0; j < grp; ++j) merge_head(p, b, hk * grp + j, np);
       if (lane == 0) atomicExch(&counters[b * p.h_kv + hk], 0u);
     }
   }

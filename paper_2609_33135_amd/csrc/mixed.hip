@@ -7,8 +7,8 @@
 // head) counter when its state is written; the last one merges the group's
 // query heads (log-sum-exp, the same arithmetic as the separate merge kernel)
 // and resets the counter, so the step needs no second launch.  A workgroup is
-// 512 threads with 128 KB of LDS: two prefill tile buffers, or eight 16 KB
-// decode V slabs.
+// 512 threads; a prefill item uses about 98 KB of LDS for its two tile buffers, a
+// group of eight decode items none (their K and V go straight to registers).
 //
 // Placement: a prefill workgroup holds a whole compute unit (its LDS and all
 // of its registers), so prefill and decode cannot share a unit at the same
@@ -23,8 +23,7 @@ namespace mpfa {
 
 namespace {
 
-constexpr int kMixedLds = 8 * kVBytes;
-static_assert(sizeof(PrefillSmemT<kPvFp8>) * 2 <= kMixedLds, "prefill tiles must fit the mixed LDS");
+constexpr int kMixedLds = sizeof(PrefillSmemT<kPvFp8>) * 2;
 
 // Blocks are dealt to the 8 XCDs round-robin, so the grid is laid out in rounds
 // of 8 consecutive blocks.  Decode rounds (8 groups of 8 decode work items)
@@ -57,7 +56,7 @@ __global__ __launch_bounds__(512, 1) void mixed_kernel(MixedParams m) {
   const int hk = (item / p.max_partitions) % p.h_kv;
   const int b = item / (p.max_partitions * p.h_kv);
   if (b >= p.batch) return;
-  decode_partition<SMOOTH, MX, true>(p, b, hk, part, lds + wave * kVBytes, m.counters);
+  decode_partition<SMOOTH, MX, true>(p, b, hk, part, m.counters);
 }
 
 }  // namespace
