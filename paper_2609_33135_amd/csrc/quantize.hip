@@ -50,6 +50,11 @@ __device__ __forceinline__ float* partial_ptr(const QuantParams& p, int64_t t0, 
   return reinterpret_cast<float*>(base);
 }
 
+// the per-head arrival counters (uint32 [hs]) and slice amaxes (float [hs][4])
+__device__ __forceinline__ uint8_t* fin_scratch(const QuantParams& p, int64_t t0, int hs) {
+  return p.q_codes + t0 * (int64_t)p.h_q * 64 + (int64_t)6 * hs * kD * 4;
+}
+
 // mean of head hh (0..h_q-1: Q, then K) and its BF16 output row
 __device__ __forceinline__ uint16_t* mean_row(const QuantParams& p, int b, int hh) {
   return hh < p.h_q ? p.q_mean + ((int64_t)b * p.h_q + hh) * kD
@@ -71,6 +76,8 @@ __global__ __launch_bounds__(256) void stats_partial_kernel(QuantParams p) {
   const StatsShape ss = stats_shape(p);
   const int tb = blk * 128, te = min(n, tb + 128);
   const int nunits = ss.hs * 16;
+  if (nblk >= 2 && blk == 0)   // arrival counters of stats_final_kernel
+    for (int i = threadIdx.x; i < ss.hs; i += blockDim.x) reinterpret_cast<uint32_t*>(fin_scratch(p, t0, ss.hs))[i] = 0u;
   for (int u0 = 0; u0 < nunits; u0 += 256 * kStatUnits) {
     const uint4* src[kStatUnits];
     int64_t stride[kStatUnits];   // in 16-byte words per token
@@ -158,124 +165,163 @@ __global__ __launch_bounds__(256) void stats_partial_kernel(QuantParams p) {
   }
 }
 
-// One workgroup of 512 threads per (head, sequence): block partials added in
-// block order, FP32 divide, BF16 rounding; tensor scale from the per-channel
-// max / min.  Also covers sequences with no tokens and the calls that need no
-// per-token statistics at all (need_partials == 0).  The partials arrive in
-// LDS 64 blocks at a time, loaded by all threads (coalesced 512-byte rows, the
-// next chunk in flight while the current one is added); threads 0..127 own one
-// channel each and add its partials strictly in block order.
-constexpr int kFinThreads = 512;
-constexpr int kFinChunk = 64;                                      // blocks per chunk
-constexpr int kFinLoads = 3 * kFinChunk * (kD / 4) / kFinThreads;  // float4 loads per thread and chunk
+// stats_final_kernel: one workgroup of 256 threads per (head, 32-channel
+// slice, sequence), so that the partials of one head are read by four compute
+// units.  The slice's partials arrive in LDS 256 blocks at a time (coalesced
+// 128-byte rows, the next chunk in flight while the current one is added);
+// threads 0..31 own one channel each and add its partials strictly in block
+// order, then FP32 divide and BF16 rounding.  The tensor scale needs the amax
+// of the whole head: each slice stores its own and counts itself in the
+// head's arrival counter; the fourth arrival takes the maximum and writes the
+// scale.  Counters and slice amaxes live in the spare bytes of the first
+// block's q_codes rows (zeroed by stats_partial_kernel), which the quantizer
+// overwrites later.  Sequences whose statistics need no partials (frozen
+// statistics, empty or one-block sequences) are handled by slice 0 alone.
+constexpr int kFinThreads = 256;
+constexpr int kFinSlice = 32;                                        // channels per workgroup
+constexpr int kFinChunk = 256;                                       // blocks per chunk
+constexpr int kFinLoads = 3 * kFinChunk * (kFinSlice / 4) / kFinThreads;   // float4 loads per thread and chunk
 
-__device__ __forceinline__ void fin_load(const QuantParams& p, int64_t t0, int nblk, int hs, int hh, int blk0,
-                                         float4 (&r)[kFinLoads]) {
+__device__ __forceinline__ void fin_load(const QuantParams& p, int64_t t0, int nblk, int hs, int hh, int c0,
+                                         int blk0, float4 (&r)[kFinLoads]) {
 #pragma unroll
   for (int i = 0; i < kFinLoads; ++i) {
     const int idx = i * kFinThreads + (int)threadIdx.x;
-    const int arr = idx / (kFinChunk * (kD / 4)), rem = idx % (kFinChunk * (kD / 4));
-    const int blk = blk0 + rem / (kD / 4), q4 = rem % (kD / 4);
+    const int arr = idx / (kFinChunk * (kFinSlice / 4)), rem = idx % (kFinChunk * (kFinSlice / 4));
+    const int blk = blk0 + rem / (kFinSlice / 4), q4 = rem % (kFinSlice / 4);
     r[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (blk < nblk)
       r[i] = *reinterpret_cast<const float4*>(partial_ptr(p, t0, nblk, blk, hs) + (int64_t)arr * hs * kD + hh * kD +
-                                              4 * q4);
+                                              c0 + 4 * q4);
   }
 }
 
 __global__ __launch_bounds__(kFinThreads) void stats_final_kernel(QuantParams p) {
-  __shared__ float4 chunk[3 * kFinChunk * (kD / 4)];   // [sum, max, min][block][channel / 4]: 96 KB
-  __shared__ float red[2];
-  const int hh = blockIdx.x, b = blockIdx.y, t = threadIdx.x, c = t;
+  __shared__ float4 chunk[3 * kFinChunk * (kFinSlice / 4)];   // [sum, max, min][block][channel / 4]: 96 KB
+  __shared__ float red[4];
+  const int hh = blockIdx.x >> 2, slice = blockIdx.x & 3, b = blockIdx.y, t = threadIdx.x;
   const int64_t t0 = p.cu_seqlens[b];
   const int n = p.cu_seqlens[b + 1] - (int)t0;
   const int nblk = (n + 127) >> 7;
   if (p.need_partials && nblk == 1) return;   // finished by stats_partial_kernel
   const StatsShape ss = stats_shape(p);
-  float tot = 0.0f, mx = -INFINITY, mn = INFINITY;
   const bool have = p.need_partials && nblk >= 2;
-  if (have) {
+  if (!have) {
+    // no partials: the (frozen or zero) means and a zero amax, by slice 0
+    if (slice != 0) return;
+    if (t < kD) {
+      uint16_t* mrow = mean_row(p, b, hh);
+      uint16_t m = 0;
+      if (!p.compute_stats && p.smooth) m = mrow[t];
+      if (p.compute_stats) mrow[t] = m;
+    }
+    if (t == 0) write_tscale(p, b, hh, 0.0f);
+    return;
+  }
+  const int c0 = slice * kFinSlice, c = c0 + t;
+  float tot = 0.0f, mx = -INFINITY, mn = INFINITY;
+  {
     float4 r[kFinLoads];
-    fin_load(p, t0, nblk, ss.hs, hh, 0, r);
+    fin_load(p, t0, nblk, ss.hs, hh, c0, 0, r);
     for (int blk0 = 0; blk0 < nblk; blk0 += kFinChunk) {
 #pragma unroll
       for (int i = 0; i < kFinLoads; ++i) chunk[i * kFinThreads + t] = r[i];
       __syncthreads();
-      if (blk0 + kFinChunk < nblk) fin_load(p, t0, nblk, ss.hs, hh, blk0 + kFinChunk, r);
-      if (c < kD) {
+      if (blk0 + kFinChunk < nblk) fin_load(p, t0, nblk, ss.hs, hh, c0, blk0 + kFinChunk, r);
+      if (t < kFinSlice) {
         const float* cs = reinterpret_cast<const float*>(chunk);
         const int nb = min(kFinChunk, nblk - blk0);
         for (int j = 0; j < nb; ++j) {
-          tot += cs[j * kD + c];
-          mx = fmaxf(mx, cs[(kFinChunk + j) * kD + c]);
-          mn = fminf(mn, cs[(2 * kFinChunk + j) * kD + c]);
+          tot += cs[j * kFinSlice + t];
+          mx = fmaxf(mx, cs[(kFinChunk + j) * kFinSlice + t]);
+          mn = fminf(mn, cs[(2 * kFinChunk + j) * kFinSlice + t]);
         }
       }
       __syncthreads();
     }
   }
-  float amax = 0.0f;
-  if (c < kD) {
-    uint16_t* mrow = mean_row(p, b, hh);
-    uint16_t m = 0;
-    if (ss.want_sum && n > 0) m = bf16_rne(__fdiv_rn(tot, (float)n));
-    else if (!p.compute_stats && p.smooth) m = mrow[c];
-    if (p.compute_stats) mrow[c] = m;
-    const float mu = bf16_to_f32(m);
-    amax = have ? fmaxf(__builtin_fabsf(mx - mu), __builtin_fabsf(mn - mu)) : 0.0f;
-    for (int off = 32; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
-    if ((c & 63) == 0) red[c >> 6] = amax;
+  if (t < 64) {   // one wave: the slice's 32 channels
+    float amax = 0.0f;
+    if (t < kFinSlice) {
+      uint16_t* mrow = mean_row(p, b, hh);
+      uint16_t m = 0;
+      if (ss.want_sum) m = bf16_rne(__fdiv_rn(tot, (float)n));
+      else if (!p.compute_stats && p.smooth) m = mrow[c];
+      if (p.compute_stats) mrow[c] = m;
+      const float mu = bf16_to_f32(m);
+      amax = fmaxf(__builtin_fabsf(mx - mu), __builtin_fabsf(mn - mu));
+    }
+    for (int off = 16; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
+    if (t == 0) {
+      uint8_t* scr = fin_scratch(p, t0, ss.hs);
+      uint32_t* cnt = reinterpret_cast<uint32_t*>(scr) + hh;
+      float* samax = reinterpret_cast<float*>(scr + ss.hs * 4) + hh * 4;
+      samax[slice] = amax;
+      // release: the slice amax is visible before the arrival is counted
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      if (atomicAdd(cnt, 1u) == 3u) {   // the head's last slice
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        const float a = fmaxf(fmaxf(samax[0], samax[1]), fmaxf(samax[2], samax[3]));
+        write_tscale(p, b, hh, a);
+      }
+    }
   }
-  __syncthreads();
-  if (c == 0) write_tscale(p, b, hh, fmaxf(red[0], red[1]));
 }
 
-// NVFP4 quantization of one 16-channel group held as 16 centered FP32 values:
-// returns 8 code bytes (as a 64-bit word, low nibble first) and the scale byte.
+// NVFP4 quantization (Sec. 2.1 Eq. 1) of a 16-channel group of centered FP32
+// values, in two steps so that the group may be spread over lanes: the scale
+// from the group amax, then the codes of 8 channels at a time.
 // rcp_sd[c] = RN(1 / e4m3_value(c)) for the positive E4M3 codes; with a
 // power-of-two t, RN(1 / (t * sd)) = rcp_sd / t and RN(1 / (6 t)) = RN(1/6) / t.
+struct Nv4Scale {
+  uint32_t code;   // E4M3 scale byte
+  float scale;     // t * sd (exact)
+  float r;         // RN(1 / scale)
+  int mode;        // 0: all codes are signed zeros; 1: product quotients; 2: IEEE division
+};
 
+__device__ __forceinline__ Nv4Scale nvfp4_scale(float a, float t, const float* rcp_sd) {
+  const int kt = ilog2f(t);
+  float q = div_by_scale(a, 6.0f * t, __builtin_ldexpf(kRcp6, -kt));   // RN(amax / (6 t))
+  if (!(q < 0x1p100f)) q = 0x1p100f;   // an overflowing quotient saturates like +inf would
+  Nv4Scale s;
+  s.code = fp8_sat_pair(0u, q, 0.0f, false) & 0xFFu;                   // E4M3_RNE_sat
+  const float sd = e4m3_value(s.code);
+  s.scale = t * sd;   // exact: t is a power of two
+  s.r = __builtin_ldexpf(rcp_sd[s.code], -kt);
+  // quotients near the FP32 range (a frozen K tensor scale far below a later
+  // token) take the IEEE division and the saturating encoder
+  s.mode = sd == 0.0f ? 0 : (a * s.r < 0x1p100f ? 1 : 2);
+  return s;
+}
+
+// Codes of 8 channels (element i in nibble i) under the group scale s.
+__device__ __forceinline__ uint32_t nvfp4_encode8(const float* x, const Nv4Scale& s) {
+  uint32_t w = 0;
+  if (s.mode == 0) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w |= ((__float_as_uint(x[i]) >> 28) & 8u) << (4 * i);
+  } else if (s.mode == 1) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      w = fp4_pair(w, div_by_scale(x[2 * j], s.scale, s.r), div_by_scale(x[2 * j + 1], s.scale, s.r), 1.0f, j);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w |= e2m1_rne_sat(__fdiv_rn(x[i], s.scale)) << (4 * i);
+  }
+  return w;
+}
+
+// One whole group: 8 code bytes (as a 64-bit word, low nibble first) and the
+// scale byte.
 __device__ __forceinline__ uint64_t nvfp4_group(const float* xc, float t, const float* rcp_sd,
                                                 uint32_t* scale_code) {
   float a = 0.0f;
 #pragma unroll
   for (int i = 0; i < 16; ++i) a = fmaxf(a, __builtin_fabsf(xc[i]));
-  const int kt = ilog2f(t);
-  float q = div_by_scale(a, 6.0f * t, __builtin_ldexpf(kRcp6, -kt));   // RN(amax / (6 t))
-  if (!(q < 0x1p100f)) q = 0x1p100f;   // an overflowing quotient saturates like +inf would
-  const uint32_t s = fp8_sat_pair(0u, q, 0.0f, false) & 0xFFu;         // E4M3_RNE_sat
-  *scale_code = s;
-  const float sd = e4m3_value(s);
-  uint32_t w0 = 0, w1 = 0;
-  if (sd == 0.0f) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      w0 |= ((__float_as_uint(xc[i]) >> 28) & 8u) << (4 * i);
-      w1 |= ((__float_as_uint(xc[8 + i]) >> 28) & 8u) << (4 * i);
-    }
-  } else {
-    const float scale = t * sd;   // exact: t is a power of two
-    const float r = __builtin_ldexpf(rcp_sd[s], -kt);
-    if (a * r < 0x1p100f) {
-      float y[16];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) y[i] = div_by_scale(xc[i], scale, r);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        w0 = fp4_pair(w0, y[2 * j], y[2 * j + 1], 1.0f, j);
-        w1 = fp4_pair(w1, y[8 + 2 * j], y[8 + 2 * j + 1], 1.0f, j);
-      }
-    } else {
-      // quotients near the FP32 range (a frozen K tensor scale far below a
-      // later token): IEEE division, saturating encoder
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        w0 |= e2m1_rne_sat(__fdiv_rn(xc[i], scale)) << (4 * i);
-        w1 |= e2m1_rne_sat(__fdiv_rn(xc[8 + i], scale)) << (4 * i);
-      }
-    }
-  }
-  return (uint64_t)w0 | ((uint64_t)w1 << 32);
+  const Nv4Scale s = nvfp4_scale(a, t, rcp_sd);
+  *scale_code = s.code;
+  return (uint64_t)nvfp4_encode8(xc, s) | ((uint64_t)nvfp4_encode8(xc + 8, s) << 32);
 }
 
 // MXFP4 quantization of one 32-channel block held as 32 centered FP32 values:
@@ -302,69 +348,174 @@ __device__ __forceinline__ u32x4 mxfp4_group(const float* xc, uint32_t* scale_co
 
 // ---------------------------------------------------------------------------
 // Quantization and cache write.  One workgroup (256 threads) per (sequence,
-// 64-token chunk).  Group u of the chunk's Q rows is at u * group_elems in the
-// packed input, so consecutive lanes read and write consecutive groups.  V:
-// when the chunk's 64 tokens fill one cache page in order (the common prefill
-// case), each lane converts two channels of all 64 tokens and writes their two
-// channel-major 64-byte page rows whole; otherwise one byte per (token,
-// channel).  Delta_S: one lane per (token, query head), K_c recomputed from the
-// BF16 row (the FP32 subtraction is exact and deterministic).
+// 64-token chunk).
+//   Q: group u of the chunk's rows is at u * group_elems in the packed input,
+//   so consecutive lanes read and write consecutive groups; each lane has the
+//   loads of several groups in flight before it quantizes them.
+//   K and Delta_S: one lane per (token, KV head) row, the lanes of a wave on
+//   consecutive tokens of one head.  The lane reads its row once; each group's
+//   centered values feed both the quantizer and the Delta_S chains, so K is
+//   read from HBM once.  Codes, scale rows and Delta_S entries of consecutive
+//   tokens are consecutive in the cache pages: the stores are contiguous.
+//   V: when the chunk's 64 tokens fill one cache page in order (the common
+//   prefill case), each lane converts two channels of all 64 tokens and writes
+//   their two channel-major 64-byte page rows whole; otherwise one byte per
+//   (token, channel).
 // ---------------------------------------------------------------------------
 constexpr int kChunk = 64;
 constexpr int kMeanStride = kD * 2 + 16;   // bytes per BF16 mean row in LDS (padded: rows on distinct banks)
 
+// 8 centered values (x - mean, FP32) of the BF16 words v and m.
+__device__ __forceinline__ void center8(const uint4 v, const uint4 m, float* xc) {
+  const uint32_t vv[4] = {v.x, v.y, v.z, v.w}, mm[4] = {m.x, m.y, m.z, m.w};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const bool lo = (e & 1) == 0;
+    const float xv = __uint_as_float(lo ? (vv[e >> 1] << 16) : (vv[e >> 1] & 0xFFFF0000u));
+    const float mv = __uint_as_float(lo ? (mm[e >> 1] << 16) : (mm[e >> 1] & 0xFFFF0000u));
+    xc[e] = xv - mv;
+  }
+}
+
+// Max over the lanes of one quantization group (lane pairs, or quads for
+// MXFP4): DPP swaps inside each quad of lanes.
 template <bool MX>
-__device__ __forceinline__ void quant_rows(const QuantParams& p, const uint16_t* x, const uint8_t* mean_base,
-                                           const float* tscale, int H, int64_t tok0, int cnt, bool to_cache,
-                                           uint8_t* codes_out, uint8_t* scales_out, const float* rcp_sd) {
-  constexpr int G = MX ? 4 : 8;          // groups per row
-  constexpr int E = MX ? 32 : 16;        // elements per group
-  constexpr int kStep = 256 / G;         // rows advanced per loop step (blockDim 256)
-  const int ngr = cnt * H * G;
-  // group u = (i * H + h) * G + g, tracked incrementally over u += 256
-  const int g = threadIdx.x % G;
-  int h = (threadIdx.x / G) % H, i = (threadIdx.x / G) / H;
-  const int di = kStep / H, dh = kStep % H;
-  for (int u = threadIdx.x; u < ngr; u += 256) {
-    const uint4* src = reinterpret_cast<const uint4*>(x + (tok0 * H) * kD) + (int64_t)u * (E / 8);
-    const uint4* mrow = reinterpret_cast<const uint4*>(mean_base + h * kMeanStride + g * E * 2);
-    float xc[E];
+__device__ __forceinline__ float group_max(float a) {
+  a = fmaxf(a, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0xB1, 0xF, 0xF, false)));  // lane ^ 1
+  if (MX) a = fmaxf(a, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x4E, 0xF, 0xF, false)));  // lane ^ 2
+  return a;
+}
+
+// Q rows: one lane per 8 channels (16 bytes) of a row, so a wave reads and
+// writes 4 whole rows; the lanes of a group (2 for NVFP4, 4 for MXFP4) share
+// its amax.  Each lane has U units in flight before it quantizes them.
+template <bool MX>
+__device__ __forceinline__ void quant_q_rows(const QuantParams& p, const uint8_t* mean_base, const float* tscale,
+                                             int64_t tok0, int cnt, const float* rcp_sd) {
+  constexpr int L = MX ? 4 : 2;          // lanes per group
+  constexpr int U = 8;                   // units per lane in flight
+  const int H = p.h_q;
+  const int nun = cnt * H * 16;          // a multiple of 16: the lanes of a group act together
+  const uint4* src = reinterpret_cast<const uint4*>(p.q + (tok0 * H) * kD);
+  for (int u0 = threadIdx.x; u0 < nun; u0 += 256 * U) {
+    uint4 v[U];
 #pragma unroll
-    for (int w = 0; w < E / 8; ++w) {
-      const uint4 v = src[w];
-      const uint4 m = p.smooth ? mrow[w] : make_uint4(0, 0, 0, 0);
-      const uint32_t vv[4] = {v.x, v.y, v.z, v.w}, mm[4] = {m.x, m.y, m.z, m.w};
+    for (int k = 0; k < U; ++k) {
+      v[k] = src[min(u0 + 256 * k, nun - 1)];   // past the end: not stored
+      // the loads issue in unit order, all before the first unit is used
+      __builtin_amdgcn_sched_barrier(0);
+    }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const bool lo = (e & 1) == 0;
-        const float xv = __uint_as_float(lo ? (vv[e >> 1] << 16) : (vv[e >> 1] & 0xFFFF0000u));
-        const float mv = __uint_as_float(lo ? (mm[e >> 1] << 16) : (mm[e >> 1] & 0xFFFF0000u));
-        xc[w * 8 + e] = xv - mv;
+    for (int k = 0; k < U; ++k) {
+      const int u = u0 + 256 * k;
+      if (u < nun) {
+        const int r = u >> 4, c8 = u & 15, h = r % H, g = c8 / L;
+        float xc[8];
+        center8(v[k], *reinterpret_cast<const uint4*>(mean_base + h * kMeanStride + c8 * 16), xc);
+        float a = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) a = fmaxf(a, __builtin_fabsf(xc[i]));
+        a = group_max<MX>(a);
+        const int64_t row = tok0 * H + r;
+        uint32_t w, sc;
+        if (MX) {
+          int e = -127;
+          if (a > 0.0f) e = max(-127, min(127, ilog2f(a) - 2));
+          sc = (uint32_t)(e + 127);
+          const float pw = __builtin_ldexpf(1.0f, max(e, -126));
+          w = 0u;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) w = fp4_pair(w, xc[2 * j], xc[2 * j + 1], pw, j);
+        } else {
+          const Nv4Scale s = nvfp4_scale(a, tscale[h], rcp_sd);
+          sc = s.code;
+          w = nvfp4_encode8(xc, s);
+        }
+        *reinterpret_cast<uint32_t*>(p.q_codes + row * 64 + c8 * 4) = w;
+        if (c8 % L == 0) {
+          p.q_scales[row * 8 + g] = (uint8_t)sc;
+          if (MX) p.q_scales[row * 8 + 4 + g] = 0;
+        }
       }
     }
-    int64_t row;   // destination row: token row of q_codes, or cache row
-    if (to_cache) {
-      const int64_t slot = p.slot_mapping[tok0 + i];
-      row = ((slot / kPage) * p.h_kv + h) * kPage + slot % kPage;
-    } else {
-      row = (tok0 + i) * H + h;
-    }
-    uint32_t sc;
-    if (MX) {
-      const u32x4 w = mxfp4_group(xc, &sc);
-      *reinterpret_cast<u32x4*>(codes_out + row * 64 + g * 16) = w;
-      scales_out[row * 8 + g] = (uint8_t)sc;
-      scales_out[row * 8 + 4 + g] = 0;
-    } else {
-      const uint64_t w = nvfp4_group(xc, tscale[h], rcp_sd, &sc);
-      *reinterpret_cast<uint64_t*>(codes_out + row * 64 + g * 8) = w;
-      scales_out[row * 8 + g] = (uint8_t)sc;
-    }
-    i += di;
-    h += dh;
-    if (h >= H) {
-      h -= H;
-      ++i;
+  }
+}
+
+// One K row: NVFP4 / MXFP4 codes and scale row into the cache, and
+// Delta_S[h] = BF16(sum_c Qbar[h][c] * K_c[c]) as an FMA chain over c from +0
+// (Eq. 9) for the query heads of the KV head's group, eight at a time.  The
+// row is read a quarter (32 channels) at a time, the next quarter's loads in
+// flight while the current one is used.
+template <bool MX>
+__device__ __forceinline__ void quant_k_rows(const QuantParams& p, const uint8_t* kmean_s, const uint8_t* qmean_s,
+                                             const float* tscale, int64_t tok0, int cnt, const float* rcp_sd) {
+  const int H = p.h_kv, grp = p.h_q / p.h_kv;
+  for (int r = threadIdx.x; r < kChunk * H; r += 256) {
+    const int i = r % kChunk, hk = r / kChunk;
+    if (i >= cnt) continue;
+    const uint4* kr = reinterpret_cast<const uint4*>(p.k + ((tok0 + i) * H + hk) * kD);
+    const uint4* km = reinterpret_cast<const uint4*>(kmean_s + hk * kMeanStride);
+    const int64_t slot = p.slot_mapping[tok0 + i];
+    const int64_t crow = ((slot / kPage) * H + hk) * kPage + slot % kPage;
+    const float t = tscale[hk];
+    uint32_t scw[2] = {0u, 0u};
+    // the first pass over the row also quantizes it
+    for (int j0 = 0; j0 == 0 || (p.smooth && j0 < grp); j0 += 8) {
+      const int nj = p.smooth ? min(8, grp - j0) : 0;
+      const uint8_t* qm = qmean_s + (hk * grp + j0) * kMeanStride;
+      float d[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) d[j] = 0.0f;
+      uint4 nxt[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) nxt[w] = kr[w];
+#pragma unroll 1
+      for (int qt = 0; qt < 4; ++qt) {   // channels 32 qt .. 32 qt + 31
+        uint4 v[4];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) v[w] = nxt[w];
+        if (qt < 3) {
+#pragma unroll
+          for (int w = 0; w < 4; ++w) nxt[w] = kr[4 * (qt + 1) + w];
+        }
+        float xc[32];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) center8(v[w], km[4 * qt + w], xc + 8 * w);
+        if (j0 == 0) {
+          uint32_t sc;
+          if (MX) {
+            *reinterpret_cast<u32x4*>(p.k_codes + crow * 64 + qt * 16) = mxfp4_group(xc, &sc);
+            scw[0] |= sc << (8 * qt);
+          } else {
+            uint32_t sc1;
+            const uint64_t c0 = nvfp4_group(xc, t, rcp_sd, &sc);
+            const uint64_t c1 = nvfp4_group(xc + 16, t, rcp_sd, &sc1);
+            *reinterpret_cast<u32x4*>(p.k_codes + crow * 64 + qt * 16) =
+                (u32x4){(uint32_t)c0, (uint32_t)(c0 >> 32), (uint32_t)c1, (uint32_t)(c1 >> 32)};
+            scw[qt >> 1] |= (sc | (sc1 << 8)) << (16 * (qt & 1));
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          if (j < nj) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+              const uint4 qv = *reinterpret_cast<const uint4*>(qm + j * kMeanStride + (4 * qt + w) * 16);
+              const uint32_t q4[4] = {qv.x, qv.y, qv.z, qv.w};
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const float qx = __uint_as_float((e & 1) == 0 ? (q4[e >> 1] << 16) : (q4[e >> 1] & 0xFFFF0000u));
+                d[j] = __builtin_fmaf(qx, xc[8 * w + e], d[j]);
+              }
+            }
+          }
+        }
+      }
+      if (j0 == 0) *reinterpret_cast<uint2*>(p.k_scales + crow * 8) = make_uint2(scw[0], scw[1]);
+      uint16_t* dsrow = p.ds + ((slot / kPage) * p.h_q + hk * grp + j0) * kPage + slot % kPage;
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (j < nj) dsrow[(int64_t)j * kPage] = bf16_rne(d[j]);
     }
   }
 }
@@ -373,7 +524,8 @@ template <bool MX>
 __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
   __shared__ int page_start;   // 1: the chunk's tokens are slots 0, 1, ... of one page, in order
   __shared__ float rcp_sd[128];
-  extern __shared__ __attribute__((aligned(16))) uint8_t sm_mean[];   // [h_q + h_kv][kMeanStride]
+  // [h_q + h_kv][kMeanStride] BF16 mean rows, then [h_q + h_kv] tensor scales
+  extern __shared__ __attribute__((aligned(16))) uint8_t sm_mean[];
   const int b = blockIdx.y;
   const int64_t t0 = p.cu_seqlens[b];
   const int n = p.cu_seqlens[b + 1] - (int)t0;
@@ -401,15 +553,16 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
     }
     *reinterpret_cast<uint4*>(sm_mean + hh * kMeanStride + w * 16) = m;
   }
+  float* ts_s = reinterpret_cast<float*>(sm_mean + (p.h_q + p.h_kv) * kMeanStride);
+  for (int hh = tid; hh < p.h_q + p.h_kv; hh += blockDim.x)
+    ts_s[hh] = hh < p.h_q ? p.q_tscale[b * p.h_q + hh] : p.k_tscale[b * p.h_kv + (hh - p.h_q)];
   __syncthreads();
   const uint8_t* qmean_s = sm_mean;
   const uint8_t* kmean_s = sm_mean + p.h_q * kMeanStride;
 
-  // Q rows (packed output) and K rows (cache)
-  quant_rows<MX>(p, p.q, qmean_s, p.q_tscale + b * p.h_q, p.h_q, tok0, cnt,
-                 false, p.q_codes, p.q_scales, rcp_sd);
-  quant_rows<MX>(p, p.k, kmean_s, p.k_tscale + b * p.h_kv, p.h_kv, tok0, cnt,
-                 true, p.k_codes, p.k_scales, rcp_sd);
+  // Q rows (packed output); K rows (cache) with Delta_S
+  quant_q_rows<MX>(p, qmean_s, ts_s, tok0, cnt, rcp_sd);
+  quant_k_rows<MX>(p, kmean_s, qmean_s, ts_s + p.h_q, tok0, cnt, rcp_sd);
   __syncthreads();
 
   // V -> E4M3, channel-major page rows (plus the characterization copies in
@@ -486,60 +639,6 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
       if (p.pv == 1) reinterpret_cast<uint16_t*>(p.v_aux)[at] = vb;
     }
   }
-  if (!p.smooth) return;
-
-  // Delta_S[h] = BF16(sum_c Qbar[h][c] * K_c[c]) as an FMA chain over c from +0.
-  // One lane per (token, KV head): K_c is formed once and feeds the chains of
-  // up to 8 query heads of the group at a time.
-  const int grp = p.h_q / p.h_kv;
-  for (int u = tid; u < cnt * p.h_kv; u += blockDim.x) {
-    const int hk = u % p.h_kv, i = u / p.h_kv;
-    const uint4* kr = reinterpret_cast<const uint4*>(p.k + ((tok0 + i) * p.h_kv + hk) * kD);
-    const uint4* km = reinterpret_cast<const uint4*>(kmean_s + hk * kMeanStride);
-    const int64_t slot = p.slot_mapping[tok0 + i];
-    uint16_t* dsrow = p.ds + ((slot / kPage) * p.h_q + hk * grp) * kPage + slot % kPage;
-    for (int j0 = 0; j0 < grp; j0 += 8) {
-      const int nj = min(8, grp - j0);
-      const uint8_t* qm = qmean_s + (hk * grp + j0) * kMeanStride;
-      float d[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) d[j] = 0.0f;
-      for (int half = 0; half < 2; ++half) {
-        // one 128-byte line of the K row per burst: a row read piecewise over a
-        // long loop gets evicted from L2 between its pieces
-        uint4 kh[8];
-#pragma unroll
-        for (int w = 0; w < 8; ++w) kh[w] = kr[half * 8 + w];
-#pragma unroll
-        for (int w = 0; w < 8; ++w) {
-          const uint4 kv = kh[w], mv = km[half * 8 + w];
-          const uint32_t k4[4] = {kv.x, kv.y, kv.z, kv.w}, m4[4] = {mv.x, mv.y, mv.z, mv.w};
-          float kc[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const bool lo = (e & 1) == 0;
-            kc[e] = __uint_as_float(lo ? (k4[e >> 1] << 16) : (k4[e >> 1] & 0xFFFF0000u)) -
-                    __uint_as_float(lo ? (m4[e >> 1] << 16) : (m4[e >> 1] & 0xFFFF0000u));
-          }
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            if (j < nj) {
-              const uint4 qv = *reinterpret_cast<const uint4*>(qm + j * kMeanStride + (half * 8 + w) * 16);
-              const uint32_t q4[4] = {qv.x, qv.y, qv.z, qv.w};
-#pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                const float qx = __uint_as_float((e & 1) == 0 ? (q4[e >> 1] << 16) : (q4[e >> 1] & 0xFFFF0000u));
-                d[j] = __builtin_fmaf(qx, kc[e], d[j]);
-              }
-            }
-          }
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (j < nj) dsrow[(int64_t)(j0 + j) * kPage] = bf16_rne(d[j]);
-    }
-  }
 }
 
 __global__ void convert_kernel(int fmt, const float* x, int64_t n, uint8_t* out) {
@@ -570,12 +669,12 @@ hipError_t launch_quantize(const QuantParams& p, hipStream_t stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  stats_final_kernel<<<dim3(hs, p.batch), dim3(kFinThreads), 0, stream>>>(p);
+  stats_final_kernel<<<dim3(hs * 4, p.batch), dim3(kFinThreads), 0, stream>>>(p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (p.total_tokens > 0 && p.max_seqlen > 0) {
     const dim3 grid((p.max_seqlen + kChunk - 1) / kChunk, p.batch);
-    const size_t lds = (size_t)(p.h_q + p.h_kv) * kMeanStride;
+    const size_t lds = (size_t)(p.h_q + p.h_kv) * (kMeanStride + sizeof(float));
     if (p.mx) quantize_kernel<true><<<grid, dim3(256), lds, stream>>>(p);
     else quantize_kernel<false><<<grid, dim3(256), lds, stream>>>(p);
     e = hipGetLastError();
