@@ -102,6 +102,9 @@ def parse():
     ap.add_argument("--cpu-rows", type=int, default=16384, help="oracle sample: query rows of head 0")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (reference for memory counters)")
+    ap.add_argument("--ablation", action="store_true",
+                    help="softmax ablation chain of the prefill (characterization library): exp2 off, "
+                         "then row max / row sum / rescale off")
     return ap.parse_args()
 
 
@@ -503,6 +506,51 @@ def cpu_baseline_decode(np, W, sd):
                       f"in {dt:.2f} s; quantization not timed"}
 
 
+def softmax_ablation(torch, np, mp, W, seq, args):
+    """Softmax stage costs of the prefill by the ablation chain (Sec. 3.2, Fig. 3c):
+    the same launch timed with the full softmax, with P = its exponent argument
+    (no exp2), and additionally without row max, row sum and O rescale.  Runs
+    the characterization library libmpfa_ablate.so (outputs meaningless by
+    design); the product library is restored afterwards."""
+    import ctypes as C
+    product = mp.LIB_PATH
+    path = os.path.join(os.path.dirname(mp.LIB_PATH), "libmpfa_ablate.so")
+    out = {"note": "HIP events, mean of --steps launches per level; costs are differences "
+                   "between levels (exp2 = full - level 1; max/sum/rescale = level 1 - level 2)"}
+    try:
+        mp.LIB_PATH = path
+        L = mp.lib()
+        L.mpfa_ablation_set_level.restype = C.c_int
+        L.mpfa_ablation_set_level.argtypes = [C.c_int]
+        for name, mx in (("nvfp4", False), ("mxfp4", True)):
+            log(f"softmax ablation chain, {name} ...")
+            st = setup_prefill(torch, np, mp, W, seq, smooth=True, mx=mx)
+            run_quant(mp, st)
+            ms = []
+            for level in (0, 1, 2):
+                assert L.mpfa_ablation_set_level(level) == 0
+                for _ in range(args.warmup):
+                    run_prefill(mp, st)
+                torch.cuda.synchronize()
+                ts = []
+                for _ in range(args.steps):
+                    with Timer(torch) as t:
+                        run_prefill(mp, st)
+                    ts.append(t)
+                ms.append(sum(t.ms() for t in ts) / args.steps)
+            L.mpfa_ablation_set_level(0)
+            out[name] = {"full_ms": ms[0], "no_exp2_ms": ms[1], "no_softmax_stats_ms": ms[2],
+                         "exp2_ms": ms[0] - ms[1], "exp2_frac": (ms[0] - ms[1]) / ms[0],
+                         "max_sum_rescale_ms": ms[1] - ms[2], "max_sum_rescale_frac": (ms[1] - ms[2]) / ms[0]}
+            log(f"  {name}: full {ms[0]:.2f} ms, exp2 {ms[0] - ms[1]:.2f} ms ({100 * (ms[0] - ms[1]) / ms[0]:.1f} %), "
+                f"max/sum/rescale {ms[1] - ms[2]:.2f} ms ({100 * (ms[1] - ms[2]) / ms[0]:.1f} %)")
+            del st
+            torch.cuda.empty_cache()
+    finally:
+        mp.LIB_PATH = product
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -655,6 +703,9 @@ def main():
                                     "quant_ms": mq_ms, "layer_ms": mq_ms + mx_ms}
             del sm
             torch.cuda.empty_cache()
+
+    if args.ablation:
+        res["softmax_ablation"] = softmax_ablation(torch, np, mp, W, seq, args)
 
     if not args.no_prefill and not args.no_sweep:
         # Llama-3.1-8B-shaped prefill over the paper's range of lengths (Sec. 7.2

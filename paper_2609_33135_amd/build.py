@@ -18,6 +18,10 @@ LIB = os.path.join(PKG, "libmpfa.so")
 SOURCES = ["api.cpp", "quantize.hip", "prefill.hip", "decode.hip", "mixed.hip", "debug_checks.hip"]
 DEBUG_LIB = os.path.join(PKG, "libmpfa_debug.so")
 PROBE_LIB = os.path.join(PKG, "libmpfa_probe.so")
+# characterization library: the product kernels plus the softmax ablation
+# variants of the prefill (outputs meaningless by design; only the benchmark's
+# --ablation leg loads it)
+ABLATE_LIB = os.path.join(PKG, "libmpfa_ablate.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CLANG = os.environ.get("MPFA_CLANG", "/opt/rocm/lib/llvm/bin/clang++")
 ARCH = os.environ.get("MPFA_ARCH", "gfx950")
@@ -40,9 +44,11 @@ EXTRA = {"prefill.hip": ["-fno-honor-nans"], "mixed.hip": ["-fno-honor-nans"],
          "probe.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
-def _compile(src: str, debug: bool = False) -> str:
-    out = os.path.join(BUILD, os.path.splitext(src)[0] + ("_debug" if debug else "") + ".o")
-    extra = (["-DMPFA_DEBUG_CHECKS"] if debug else []) + EXTRA.get(src, [])
+def _compile(src: str, debug: bool = False, ablate: bool = False) -> str:
+    tag = "_debug" if debug else ("_ablate" if ablate else "")
+    out = os.path.join(BUILD, os.path.splitext(src)[0] + tag + ".o")
+    extra = (["-DMPFA_DEBUG_CHECKS"] if debug else []) + (["-DMPFA_ABLATION_BUILD"] if ablate else []) + \
+        EXTRA.get(src, [])
     cmd = [CLANG, "-x", "hip", *COMMON, *extra, "-c", os.path.join(CSRC, src), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
@@ -65,18 +71,21 @@ def _link(out: str, objs: list[str]) -> None:
 
 def build(verbose: bool = False) -> str:
     """Compile every source, then link libmpfa.so, libmpfa_debug.so (the same
-    kernels; its entry points also check the data they are handed) and the
-    benchmark's probe library."""
+    kernels; its entry points also check the data they are handed), the
+    benchmark's probe library and its characterization library."""
     os.makedirs(BUILD, exist_ok=True)
-    jobs = [(s, False) for s in SOURCES] + [("api.cpp", True), ("probe.hip", False)]
+    jobs = [(s, False, False) for s in SOURCES] + [("api.cpp", True, False), ("probe.hip", False, False),
+                                                   ("prefill.hip", False, True)]
     with ThreadPoolExecutor(max_workers=len(jobs)) as ex:
         objs = list(ex.map(lambda j: _compile(*j), jobs))
     kernels = objs[1:len(SOURCES)]
     _link(LIB, [objs[0], *kernels])
     _link(DEBUG_LIB, [objs[len(SOURCES)], *kernels])
     _link(PROBE_LIB, [objs[len(SOURCES) + 1]])
+    ablate_prefill = objs[len(SOURCES) + 2]
+    _link(ABLATE_LIB, [objs[0], *[ablate_prefill if k.endswith("/prefill.o") else k for k in kernels]])
     if verbose:
-        print("built", LIB, DEBUG_LIB, PROBE_LIB)
+        print("built", LIB, DEBUG_LIB, PROBE_LIB, ABLATE_LIB)
     return LIB
 
 

@@ -25,18 +25,45 @@ namespace mpfa {
 
 namespace {
 
-template <int SEED, bool MX, int PV>
+template <int SEED, bool MX, int PV, int ABL = 0>
 __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(PrefillParams p) {
   __shared__ __attribute__((aligned(16))) PrefillSmemT<PV> smem[2];
-  prefill_item<SEED, MX, PV>(p, blockIdx.x, smem);
+  prefill_item<SEED, MX, PV, ABL>(p, blockIdx.x, smem);
 }
 
+#ifdef MPFA_ABLATION_BUILD
+// Characterization library only: softmax ablation level of the method's
+// kernels (compensation as accumulator input, FP8 PV), see softmax_tile.
+int g_ablation = 0;
+#endif
+
 }  // namespace
+
+#ifdef MPFA_ABLATION_BUILD
+// declared in include/mpfa_ablate.h
+extern "C" int mpfa_ablation_set_level(int level) {
+  if (level < 0 || level > 2) return 1;
+  g_ablation = level;
+  return 0;
+}
+#endif
 
 hipError_t launch_prefill(const PrefillParams& p, hipStream_t stream) {
   const unsigned blocks = (unsigned)(p.n_qtiles * p.h_q * p.batch);
   if (blocks == 0) return hipSuccess;
   const dim3 grid(blocks), block(kThreads);
+#ifdef MPFA_ABLATION_BUILD
+  if (g_ablation > 0 && p.pv == kPvFp8 && p.smooth && !p.seed_mfma && !p.seed_elem) {
+    if (p.mx) {
+      if (g_ablation == 1) prefill_kernel<kSeedInit, true, kPvFp8, 1><<<grid, block, 0, stream>>>(p);
+      else prefill_kernel<kSeedInit, true, kPvFp8, 2><<<grid, block, 0, stream>>>(p);
+    } else {
+      if (g_ablation == 1) prefill_kernel<kSeedInit, false, kPvFp8, 1><<<grid, block, 0, stream>>>(p);
+      else prefill_kernel<kSeedInit, false, kPvFp8, 2><<<grid, block, 0, stream>>>(p);
+    }
+    return hipGetLastError();
+  }
+#endif
   if (p.pv == kPvBf16) {
     if (!p.smooth) prefill_kernel<kSeedNone, false, kPvBf16><<<grid, block, 0, stream>>>(p);
     else prefill_kernel<kSeedInit, false, kPvBf16><<<grid, block, 0, stream>>>(p);

@@ -362,7 +362,12 @@ struct PTile {
 
 // Causal mask, online softmax and P quantization of one tile (Algorithm 1,
 // softmax steps), with the rescale of O when a row maximum moved.
-template <int PV>
+// ABL > 0 only in the characterization library (built with
+// MPFA_ABLATION_BUILD), whose outputs are meaningless by design: the cost of
+// a softmax stage is the time difference to the build without it (Sec. 3.2,
+// Fig. 3c).  ABL 1: P = its exponent argument (no exp2); ABL 2: also no row
+// maximum, row sum or O rescale.
+template <int PV, int ABL = 0>
 __device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][kNB], int key0, bool need_mask, const ItemState& st,
                                              float (&m)[kNB], float (&l)[kNB], f32x4 (&o)[8][kNB], PTile& pt) {
   const int g = st.g;
@@ -399,22 +404,26 @@ __device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][kNB], int key0, bool 
       mxb = fmaxf(fmaxf(mxb, s[mb + 1][nb][0]), s[mb + 1][nb][1]);
       mxb = fmaxf(fmaxf(mxb, s[mb + 1][nb][2]), s[mb + 1][nb][3]);
     }
-    const float mx = wave_max16(fmaxf(mxa, mxb));
+    const float mx = ABL >= 2 ? 0.0f : wave_max16(fmaxf(mxa, mxb));
     const float mnew = fmaxf(m[nb], mx);
     const float muse = (mnew == -INFINITY) ? 0.0f : mnew;
     alpha[nb] = (m[nb] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m[nb] - muse) * lam2);
     m[nb] = mnew;
-    const float bias = __builtin_fmaf(-muse, lam2, kLog2PScale);
+    const float bias = ABL >= 2 ? kLog2PScale : __builtin_fmaf(-muse, lam2, kLog2PScale);
     float ps;
     float ev[8][4];
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb) {
       float e[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        e[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][nb][i], lam2, bias));
-      const float q4 = (e[0] + e[1]) + (e[2] + e[3]);
-      ps = mb == 0 ? q4 : ps + q4;
+      for (int i = 0; i < 4; ++i) {
+        const float arg = __builtin_fmaf(s[mb][nb][i], lam2, bias);
+        e[i] = ABL >= 1 ? arg : __builtin_amdgcn_exp2f(arg);
+      }
+      if (ABL < 2) {
+        const float q4 = (e[0] + e[1]) + (e[2] + e[3]);
+        ps = mb == 0 ? q4 : ps + q4;
+      }
       if (PV == kPvFp8) {
         pt.pb[nb][mb] = (int)pack_fp8x4(e[0], e[1], e[2], e[3]);
       } else {
@@ -422,7 +431,7 @@ __device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][kNB], int key0, bool 
         for (int i = 0; i < 4; ++i) ev[mb][i] = e[i];
       }
     }
-    l[nb] = alpha[nb] * l[nb] + ps;
+    if (ABL < 2) l[nb] = alpha[nb] * l[nb] + ps;
     if (PV == kPvBf16) {
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
@@ -467,7 +476,7 @@ __device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][kNB], int key0, bool 
   // rescale the O rows of a query block only when one of its maxima moved
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
-    if (__builtin_amdgcn_ballot_w64(alpha[nb] != 1.0f) != 0) {
+    if (ABL < 2 && __builtin_amdgcn_ballot_w64(alpha[nb] != 1.0f) != 0) {
 #pragma unroll
       for (int db = 0; db < 8; ++db) o[db][nb] *= alpha[nb];
     }
@@ -543,7 +552,7 @@ __device__ __forceinline__ void store_output(const PrefillParams& p, const ItemS
 // order (largest tiles first) and smem two tile buffers in LDS.  Every wave
 // runs QK, softmax and PV of a tile back to back; the next tile is fetched
 // into registers meanwhile and stored to the other buffer at the end.
-template <int SEED, bool MX, int PV>
+template <int SEED, bool MX, int PV, int ABL = 0>
 __device__ __forceinline__ void prefill_item(const PrefillParams& p, int bid, PrefillSmemT<PV>* smem) {
   ItemState st;
   if (!item_setup<MX>(p, bid, st)) return;
@@ -574,7 +583,7 @@ __device__ __forceinline__ void prefill_item(const PrefillParams& p, int bid, Pr
       f32x4 s[8][kNB];
       qk_tile<SEED, MX, PV>(s, sm, st);
       PTile ptile;
-      softmax_tile<PV>(s, key0, key0 + kTile - 1 > st.wpos_min, st, m, l, o, ptile);
+      softmax_tile<PV, ABL>(s, key0, key0 + kTile - 1 > st.wpos_min, st, m, l, o, ptile);
       pv_tile<PV>(sm, ptile, o, st);
     }
     if (j > 0) store_tile<MX, PV>(smem[(j - 1) & 1], nxt, st.seed_scale);

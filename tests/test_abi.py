@@ -29,7 +29,7 @@ def mp():
 
 def test_headers_are_covered():
     assert sorted(os.path.basename(h) for h in glob.glob(os.path.join(ROOT, "include", "*.h"))) == \
-        ["mpfa.h", "mpfa_probe.h"]
+        ["mpfa.h", "mpfa_ablate.h", "mpfa_probe.h"]
 
 
 def test_exports_every_declared_symbol(mp):
@@ -52,6 +52,22 @@ def test_probe_library_is_separate(mp):
     for n in sorted(names):
         assert hasattr(P, n), f"{n} missing from libmpfa_probe.so"
         assert not hasattr(L, n), f"{n} still exported by the product library"
+
+
+def test_ablation_library_is_separate(mp):
+    """The softmax ablation levels live in libmpfa_ablate.so (the product entry
+    points plus what include/mpfa_ablate.h declares); the product library has
+    no trace of them, and the level setter validates its argument."""
+    names = _declared("mpfa_ablate.h")
+    assert names == {"mpfa_ablation_set_level"}
+    A = C.CDLL(os.path.join(os.path.dirname(mp.LIB_PATH), "libmpfa_ablate.so"))
+    L = C.CDLL(mp.LIB_PATH)
+    for n in sorted(_declared()):
+        assert hasattr(A, n), f"{n} missing from libmpfa_ablate.so"
+    assert hasattr(A, "mpfa_ablation_set_level") and not hasattr(L, "mpfa_ablation_set_level")
+    A.mpfa_ablation_set_level.restype = C.c_int
+    assert A.mpfa_ablation_set_level(3) == 1 and A.mpfa_ablation_set_level(-1) == 1
+    assert A.mpfa_ablation_set_level(2) == 0 and A.mpfa_ablation_set_level(0) == 0
 
 
 def test_debug_library_exports_the_same_symbols(mp):
