@@ -441,6 +441,13 @@ __device__ __forceinline__ void quant_q_rows(const QuantParams& p, const uint8_t
   }
 }
 
+// codes[q] = w for a runtime q (selects, no indexed register access)
+__device__ __forceinline__ void codes_put(u32x4 (&codes)[4], int q, u32x4 w) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (i == q) codes[i] = w;
+}
+
 // One K row: NVFP4 / MXFP4 codes and scale row into the cache, and
 // Delta_S[h] = BF16(sum_c Qbar[h][c] * K_c[c]) as an FMA chain over c from +0
 // (Eq. 9) for the query heads of the KV head's group, eight at a time.  The
@@ -459,6 +466,7 @@ __device__ __forceinline__ void quant_k_rows(const QuantParams& p, const uint8_t
     const int64_t crow = ((slot / kPage) * H + hk) * kPage + slot % kPage;
     const float t = tscale[hk];
     uint32_t scw[2] = {0u, 0u};
+    u32x4 codes[4];   // the row's 64 code bytes, stored whole (partial-line stores cost write-backs)
     // the first pass over the row also quantizes it
     for (int j0 = 0; j0 == 0 || (p.smooth && j0 < grp); j0 += 8) {
       const int nj = p.smooth ? min(8, grp - j0) : 0;
@@ -484,14 +492,14 @@ __device__ __forceinline__ void quant_k_rows(const QuantParams& p, const uint8_t
         if (j0 == 0) {
           uint32_t sc;
           if (MX) {
-            *reinterpret_cast<u32x4*>(p.k_codes + crow * 64 + qt * 16) = mxfp4_group(xc, &sc);
+            const u32x4 cw = mxfp4_group(xc, &sc);
+            codes_put(codes, qt, cw);
             scw[0] |= sc << (8 * qt);
           } else {
             uint32_t sc1;
             const uint64_t c0 = nvfp4_group(xc, t, rcp_sd, &sc);
             const uint64_t c1 = nvfp4_group(xc + 16, t, rcp_sd, &sc1);
-            *reinterpret_cast<u32x4*>(p.k_codes + crow * 64 + qt * 16) =
-                (u32x4){(uint32_t)c0, (uint32_t)(c0 >> 32), (uint32_t)c1, (uint32_t)(c1 >> 32)};
+            codes_put(codes, qt, (u32x4){(uint32_t)c0, (uint32_t)(c0 >> 32), (uint32_t)c1, (uint32_t)(c1 >> 32)});
             scw[qt >> 1] |= (sc | (sc1 << 8)) << (16 * (qt & 1));
           }
         }
@@ -511,7 +519,12 @@ __device__ __forceinline__ void quant_k_rows(const QuantParams& p, const uint8_t
           }
         }
       }
-      if (j0 == 0) *reinterpret_cast<uint2*>(p.k_scales + crow * 8) = make_uint2(scw[0], scw[1]);
+      if (j0 == 0) {
+        u32x4* co = reinterpret_cast<u32x4*>(p.k_codes + crow * 64);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) co[q] = codes[q];
+        *reinterpret_cast<uint2*>(p.k_scales + crow * 8) = make_uint2(scw[0], scw[1]);
+      }
       uint16_t* dsrow = p.ds + ((slot / kPage) * p.h_q + hk * grp + j0) * kPage + slot % kPage;
 #pragma unroll
       for (int j = 0; j < 8; ++j)
@@ -577,7 +590,12 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
       const int64_t tstride = (int64_t)p.h_kv * (kD / 2);
       const int64_t crow = (page * p.h_kv + h) * kD + 2 * cp;   // channel row 2cp; 2cp+1 follows
       uint8_t* dst = p.v_codes + crow * kPage;
+      // the two 64-byte channel rows (one 128-byte line) are stored whole after
+      // all 64 tokens are converted: stores of line pieces far apart in time
+      // cost partial-line write-backs
+      u32x4 r0s[kPage / 16], r1s[kPage / 16];
       // 16 tokens at a time: 16 bytes of each of the two channel rows
+#pragma unroll
       for (int qq = 0; qq < kPage; qq += 16) {
         uint32_t w[16];
 #pragma unroll
@@ -594,8 +612,8 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
             r0[q] = a;
             r1[q] = c;
           }
-          *reinterpret_cast<u32x4*>(dst + qq) = r0;
-          *reinterpret_cast<u32x4*>(dst + kPage + qq) = r1;
+          r0s[qq / 16] = r0;
+          r1s[qq / 16] = r1;
           if (p.pv == 1) {   // BF16 rows: 16 keys of each channel, 32 bytes
             uint32_t b0[8], b1[8];
 #pragma unroll
@@ -624,6 +642,13 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantParams p) {
           *reinterpret_cast<uint64_t*>(p.v_aux + (crow + 1) * 32 + qq / 2) = c1;
           p.v_aux[aux_scales + crow * 4 + qq / 16] = (uint8_t)sc0;
           p.v_aux[aux_scales + (crow + 1) * 4 + qq / 16] = (uint8_t)sc1;
+        }
+      }
+      if (page_run) {
+#pragma unroll
+        for (int q = 0; q < kPage / 16; ++q) {
+          *reinterpret_cast<u32x4*>(dst + 16 * q) = r0s[q];
+          *reinterpret_cast<u32x4*>(dst + kPage + 16 * q) = r1s[q];
         }
       }
     }
