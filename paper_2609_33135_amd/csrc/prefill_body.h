@@ -8,10 +8,11 @@ namespace mpfa {
 
 namespace {
 
-constexpr int kWaves = 8;
-constexpr int kNB = 2;                       // 16-row query blocks per wave
-constexpr int kQRows = kWaves * kNB * 16;    // 256 query rows per workgroup
-constexpr int kThreads = kWaves * 64;
+constexpr int kQRows = 256;                  // query rows per workgroup
+constexpr int kNB = 2;                       // 16-row query blocks per wave (two waves per SIMD)
+// threads of a workgroup whose waves own NB 16-row query blocks each
+constexpr int threads_for(int nb) { return kQRows / (nb * 16) * 64; }
+constexpr int kThreads = threads_for(kNB);
 
 // Precision of the PV product: the method's FP8 (P * 448 and V in E4M3), or
 // the two other assignments compared in Sec. 3.1 / Fig. 3a, BF16 P and V, and
@@ -74,10 +75,10 @@ struct TileRegs {
   uint32_t ds;     // BF16 Delta_S of key t (threads 0..127)
 };
 
+// t: the unit of the tile (0..511) this call loads
 template <bool MX, int PV>
 __device__ __forceinline__ void fetch_tile(TileRegs<PV>& r, const PrefillParams& p, const int32_t* pt,
-                                           int hk, int h, int j, int kvl) {
-  const int t = threadIdx.x;
+                                           int hk, int h, int j, int kvl, int t) {
   // the two pages of tile j: uniform across the workgroup (scalar loads)
   const int npg = (kvl + 63) >> 6;
   const int64_t pg0 = pt[min(2 * j, npg - 1)];
@@ -136,8 +137,7 @@ __device__ __forceinline__ void fetch_tile(TileRegs<PV>& r, const PrefillParams&
 }
 
 template <bool MX, int PV>
-__device__ __forceinline__ void store_tile(PrefillSmemT<PV>& sm, const TileRegs<PV>& r, float seed_scale) {
-  const int t = threadIdx.x;
+__device__ __forceinline__ void store_tile(PrefillSmemT<PV>& sm, const TileRegs<PV>& r, float seed_scale, int t) {
   if (MX) {
     const int key = t >> 2, qt = t & 3;
     *reinterpret_cast<u32x4*>(sm.k + key * 64 + ((qt ^ mx_swz(key)) << 4)) = r.kc;
@@ -201,24 +201,25 @@ enum SeedMode { kSeedNone = 0, kSeedMfma = 1, kSeedInit = 2, kSeedElem = 3 };
 
 // Per-item state of one wave: the work item, the query operands, the softmax
 // scale and the row positions.
+template <int NB = kNB>
 struct ItemState {
   int b, h, hk, q0, nq, qs, kvl, j_hi;
   int lane, wave, g, lr;
   int wrow0, wpos_min, wpos_max;
   bool wave_active;
   float lam2, seed_scale;
-  int pos[kNB];
-  f16x8 qop[kNB][4];   // NVFP4: exact FP16 query operands, tensor scale factored out
-  u32x4 qraw[kNB];     // MXFP4: raw codes of channels 32g .. 32g+31
-  int qscale[kNB];     // MXFP4: their E8M0 scale
+  int pos[NB];
+  f16x8 qop[NB][4];   // NVFP4: exact FP16 query operands, tensor scale factored out
+  u32x4 qraw[NB];     // MXFP4: raw codes of channels 32g .. 32g+31
+  int qscale[NB];     // MXFP4: their E8M0 scale
   bf16x8 bseed;        // B operand of the rank-one seed MFMA: 1 in slot 0 of lanes 0..15
 };
 
 // Decode work item `bid` (largest query tiles first, longest-processing-time
 // order) and load the wave's query operands.  Returns false when the item has
 // no rows.
-template <bool MX>
-__device__ __forceinline__ bool item_setup(const PrefillParams& p, int bid, ItemState& st) {
+template <bool MX, int NB = kNB>
+__device__ __forceinline__ bool item_setup(const PrefillParams& p, int bid, ItemState<NB>& st) {
   int b, h, rank;
   if (p.xcd_remap) {
     // block ids are dealt round-robin to the 8 XCDs; give each XCD the query
@@ -264,16 +265,16 @@ __device__ __forceinline__ bool item_setup(const PrefillParams& p, int bid, Item
   st.lam2 = __builtin_ldexpf(p.lam, eqk);        // lambda * tQ * tK
   st.seed_scale = __builtin_ldexpf(1.0f, -eqk);  // Delta_S in accumulator units
 
-  st.wrow0 = r0 + st.wave * (kNB * 16);
+  st.wrow0 = r0 + st.wave * (NB * 16);
   st.wave_active = st.wrow0 < nq;
   st.wpos_min = st.qs + st.wrow0;
-  st.wpos_max = st.qs + min(st.wrow0 + kNB * 16, nq) - 1;
+  st.wpos_max = st.qs + min(st.wrow0 + NB * 16, nq) - 1;
 
   // ---- Q operands (B of S^T = K Q^T).  NVFP4: exact FP16, tensor scale
   // factored out.  MXFP4: the raw codes of channels 32g .. 32g+31 and their
   // E8M0 scale (the lane's 32-element block of the scaled FP4 MFMA).
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
+  for (int nb = 0; nb < NB; ++nb) {
     const int row = st.wrow0 + nb * 16 + st.lr;
     st.pos[nb] = st.qs + row;
     const bool valid = row < nq;
@@ -298,8 +299,8 @@ __device__ __forceinline__ bool item_setup(const PrefillParams& p, int bid, Item
 }
 
 // S^T = seed + K Q^T of the tile in sm (Algorithm 1, scores of one tile).
-template <int SEED, bool MX, int PV>
-__device__ __forceinline__ void qk_tile(f32x4 (&s)[8][kNB], const PrefillSmemT<PV>& sm, const ItemState& st) {
+template <int SEED, bool MX, int PV, int NB = kNB>
+__device__ __forceinline__ void qk_tile(f32x4 (&s)[8][NB], const PrefillSmemT<PV>& sm, const ItemState<NB>& st) {
   const int g = st.g, lr = st.lr;
   // rank-one seed operands: every lane reads the 8 values of its row lr;
   // only reduction slot 0 of lanes 0..15 meets a nonzero B element, so the
@@ -318,7 +319,7 @@ __device__ __forceinline__ void qk_tile(f32x4 (&s)[8][kNB], const PrefillSmemT<P
       seed = *reinterpret_cast<const f32x4*>(&sm.ds[32 * g + 4 * mb]);
     }
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = seed;
+    for (int nb = 0; nb < NB; ++nb) s[mb][nb] = seed;
   }
   if (MX) {
     // one scaled FP4 MFMA per 16x16 block covers all 128 channels
@@ -329,7 +330,7 @@ __device__ __forceinline__ void qk_tile(f32x4 (&s)[8][kNB], const PrefillSmemT<P
       const u32x4 kop = *reinterpret_cast<const u32x4*>(sm.k + krow * 64 + ((g ^ mx_swz(krow)) << 4));
       const int sk = (int)((ks8 >> (8 * mb)) & 0xFFu);
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_fp4(kop, st.qraw[nb], s[mb][nb], sk, st.qscale[nb]);
+      for (int nb = 0; nb < NB; ++nb) s[mb][nb] = mfma_fp4(kop, st.qraw[nb], s[mb][nb], sk, st.qscale[nb]);
     }
   } else {
 #pragma unroll
@@ -341,13 +342,13 @@ __device__ __forceinline__ void qk_tile(f32x4 (&s)[8][kNB], const PrefillSmemT<P
           const int krow = 32 * (lr >> 2) + 4 * mb + (lr & 3);
           const f16x8 kop = *reinterpret_cast<const f16x8*>(sm.k + krow * 256 + (((4 * ks + g) ^ lr) << 4));
 #pragma unroll
-          for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = mfma_f16(kop, st.qop[nb][ks], s[mb][nb]);
+          for (int nb = 0; nb < NB; ++nb) s[mb][nb] = mfma_f16(kop, st.qop[nb][ks], s[mb][nb]);
         }
       }
   }
   if (SEED == kSeedElem) {
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) s[mb][nb] += *reinterpret_cast<const f32x4*>(&sm.ds[32 * g + 4 * mb]);
   }
@@ -355,9 +356,10 @@ __device__ __forceinline__ void qk_tile(f32x4 (&s)[8][kNB], const PrefillSmemT<P
 
 // P operands of the PV product of one tile: FP8 words (kPvFp8) or eight
 // BF16 / exact FP16 values per MFMA (kPvBf16, kPvNvfp4).
+template <int NB = kNB>
 struct PTile {
-  i32x8 pb[kNB];
-  f16x8 ph[kNB][4];   // keys 32g + 8kk .. +7
+  i32x8 pb[NB];
+  f16x8 ph[NB][4];   // keys 32g + 8kk .. +7
 };
 
 // Causal mask, online softmax and P quantization of one tile (Algorithm 1,
@@ -367,15 +369,15 @@ struct PTile {
 // a softmax stage is the time difference to the build without it (Sec. 3.2,
 // Fig. 3c).  ABL 1: P = its exponent argument (no exp2); ABL 2: also no row
 // maximum, row sum or O rescale.
-template <int PV, int ABL = 0>
-__device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][kNB], int key0, bool need_mask, const ItemState& st,
-                                             float (&m)[kNB], float (&l)[kNB], f32x4 (&o)[8][kNB], PTile& pt) {
+template <int PV, int ABL = 0, int NB = kNB>
+__device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][NB], int key0, bool need_mask, const ItemState<NB>& st,
+                                             float (&m)[NB], float (&l)[NB], f32x4 (&o)[8][NB], PTile<NB>& pt) {
   const int g = st.g;
   const float lam2 = st.lam2;
   if (need_mask) {
     // key 32g + 4mb + i of the tile lies after query position pos
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) {
+    for (int nb = 0; nb < NB; ++nb) {
       const int lim = st.pos[nb] - key0 - 32 * g;
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) {
@@ -392,9 +394,9 @@ __device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][kNB], int key0, bool 
   // 2688 = 6 * 448 (NVFP4: the largest P, 1, maps to the top E2M1 code
   // under the largest E4M3 scale)
   constexpr float kLog2PScale = PV == kPvFp8 ? kLog2_448 : (PV == kPvBf16 ? 0.0f : 11.392317422778760f);
-  float alpha[kNB];
+  float alpha[NB];
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
+  for (int nb = 0; nb < NB; ++nb) {
     // two independent chains of v_max3 (two new scores per instruction)
     float mxa = -INFINITY, mxb = -INFINITY;
 #pragma unroll
@@ -475,7 +477,7 @@ __device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][kNB], int key0, bool 
   }
   // rescale the O rows of a query block only when one of its maxima moved
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
+  for (int nb = 0; nb < NB; ++nb) {
     if (ABL < 2 && __builtin_amdgcn_ballot_w64(alpha[nb] != 1.0f) != 0) {
 #pragma unroll
       for (int db = 0; db < 8; ++db) o[db][nb] *= alpha[nb];
@@ -484,9 +486,9 @@ __device__ __forceinline__ void softmax_tile(f32x4 (&s)[8][kNB], int key0, bool 
 }
 
 // O^T += V^T P^T with V of the tile in sm.
-template <int PV>
-__device__ __forceinline__ void pv_tile(const PrefillSmemT<PV>& sm, const PTile& pt, f32x4 (&o)[8][kNB],
-                                        const ItemState& st) {
+template <int PV, int NB = kNB>
+__device__ __forceinline__ void pv_tile(const PrefillSmemT<PV>& sm, const PTile<NB>& pt, f32x4 (&o)[8][NB],
+                                        const ItemState<NB>& st) {
   const int g = st.g, lr = st.lr;
   if (PV == kPvFp8) {
 #pragma unroll
@@ -499,7 +501,7 @@ __device__ __forceinline__ void pv_tile(const PrefillSmemT<PV>& sm, const PTile&
       const i32x8 vop = {(int)va[0], (int)va[1], (int)va[2], (int)va[3],
                          (int)vb[0], (int)vb[1], (int)vb[2], (int)vb[3]};
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) o[db][nb] = mfma_fp8(vop, pt.pb[nb], o[db][nb]);
+      for (int nb = 0; nb < NB; ++nb) o[db][nb] = mfma_fp8(vop, pt.pb[nb], o[db][nb]);
     }
   } else {
     // four 32-key MFMAs per channel block: MFMA kk reduces keys 32g + 8kk .. +7
@@ -512,7 +514,7 @@ __device__ __forceinline__ void pv_tile(const PrefillSmemT<PV>& sm, const PTile&
       for (int kk = 0; kk < 4; ++kk) {
         const u32x4 va = *reinterpret_cast<const u32x4*>(vr + (((4 * g + kk) ^ lr) << 4));
 #pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) {
+        for (int nb = 0; nb < NB; ++nb) {
           if (PV == kPvBf16)
             o[db][nb] = mfma_bf16(__builtin_bit_cast(bf16x8, va), __builtin_bit_cast(bf16x8, pt.ph[nb][kk]),
                                   o[db][nb]);
@@ -526,10 +528,11 @@ __device__ __forceinline__ void pv_tile(const PrefillSmemT<PV>& sm, const PTile&
 
 // out = O / (448 l) as BF16 (for the other PV precisions the factor is the
 // one their P carries).
-__device__ __forceinline__ void store_output(const PrefillParams& p, const ItemState& st, const float (&l)[kNB],
-                                             const f32x4 (&o)[8][kNB]) {
+template <int NB = kNB>
+__device__ __forceinline__ void store_output(const PrefillParams& p, const ItemState<NB>& st, const float (&l)[NB],
+                                             const f32x4 (&o)[8][NB]) {
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
+  for (int nb = 0; nb < NB; ++nb) {
     const float lt = wave_sum16(l[nb]);
     const int row = st.wrow0 + nb * 16 + st.lr;
     if (row < st.nq) {
@@ -554,7 +557,7 @@ __device__ __forceinline__ void store_output(const PrefillParams& p, const ItemS
 // into registers meanwhile and stored to the other buffer at the end.
 template <int SEED, bool MX, int PV, int ABL = 0>
 __device__ __forceinline__ void prefill_item(const PrefillParams& p, int bid, PrefillSmemT<PV>* smem) {
-  ItemState st;
+  ItemState<> st;
   if (!item_setup<MX>(p, bid, st)) return;
 
   float m[kNB], l[kNB];
@@ -570,23 +573,23 @@ __device__ __forceinline__ void prefill_item(const PrefillParams& p, int bid, Pr
   const int32_t* pt = p.page_table + (int64_t)st.b * p.max_pages;
   {
     TileRegs<PV> r0r;
-    fetch_tile<MX, PV>(r0r, p, pt, st.hk, st.h, st.j_hi, st.kvl);
-    store_tile<MX, PV>(smem[st.j_hi & 1], r0r, st.seed_scale);
+    fetch_tile<MX, PV>(r0r, p, pt, st.hk, st.h, st.j_hi, st.kvl, threadIdx.x);
+    store_tile<MX, PV>(smem[st.j_hi & 1], r0r, st.seed_scale, threadIdx.x);
   }
   __syncthreads();
   for (int j = st.j_hi; j >= 0; --j) {
     TileRegs<PV> nxt;
-    if (j > 0) fetch_tile<MX, PV>(nxt, p, pt, st.hk, st.h, j - 1, st.kvl);
+    if (j > 0) fetch_tile<MX, PV>(nxt, p, pt, st.hk, st.h, j - 1, st.kvl, threadIdx.x);
     const PrefillSmemT<PV>& sm = smem[j & 1];
     const int key0 = j * kTile;
     if (st.wave_active && key0 <= st.wpos_max) {
       f32x4 s[8][kNB];
       qk_tile<SEED, MX, PV>(s, sm, st);
-      PTile ptile;
+      PTile<> ptile;
       softmax_tile<PV, ABL>(s, key0, key0 + kTile - 1 > st.wpos_min, st, m, l, o, ptile);
       pv_tile<PV>(sm, ptile, o, st);
     }
-    if (j > 0) store_tile<MX, PV>(smem[(j - 1) & 1], nxt, st.seed_scale);
+    if (j > 0) store_tile<MX, PV>(smem[(j - 1) & 1], nxt, st.seed_scale, threadIdx.x);
     __syncthreads();
   }
 
