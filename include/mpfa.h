@@ -342,8 +342,11 @@ mpfa_status mpfa_mixed_step(const mpfa_prefill_args* prefill, const mpfa_decode_
  * 1..126, a positive E4M3 code) = the E2M1 code of x / e4m3(c) exactly as the
  * NVFP4 quantizer forms it (the correctly rounded quotient, then E2M1);
  * 0x200 + b (b = 1..254) = the E2M1 code of x / 2^(b - 127) as the MXFP4
- * quantizer forms it.  x and out are device pointers of n elements;
- * MPFA_ERR_INVALID for another fmt. */
+ * quantizer forms it; 0x300 + c and 0x400 + b = the same two quotients
+ * written out from their definitions (IEEE division __fdiv_rn, exact
+ * power-of-two scaling ldexpf, then the fmt 1 encoder), the references the
+ * quantizer's element paths are checked against.  x and out are device
+ * pointers of n elements; MPFA_ERR_INVALID for another fmt. */
 mpfa_status mpfa_convert(int32_t fmt, const float* x, int64_t n, uint8_t* out,
                          mpfa_stream_t stream);
 

@@ -299,5 +299,7 @@ def convert(fmt: int, x, out, stream=None):
     """mpfa_convert: fmt 0 FP32 -> E4M3, fmt 1 FP32 -> E2M1 (one code per byte),
     written from the format definitions; fmt 2 / 3 the same through the hardware
     converters the quantization pass uses; 0x100 + c: E2M1 of x / e4m3(c) by the
-    NVFP4 quantizer's division; 0x200 + b: E2M1 of x / 2^(b-127) (MXFP4)."""
+    NVFP4 quantizer's division; 0x200 + b: E2M1 of x / 2^(b-127) (MXFP4);
+    0x300 + c / 0x400 + b: the same quotients from their definitions (IEEE
+    division, exact scaling) through the fmt 1 encoder."""
     _check(lib().mpfa_convert(fmt, _ptr(x), x.numel(), _ptr(out), _stream(stream)), "mpfa_convert")

@@ -436,7 +436,8 @@ mpfa_status mpfa_mixed_step(const mpfa_prefill_args* prefill, const mpfa_decode_
 
 
 mpfa_status mpfa_convert(int32_t fmt, const float* x, int64_t n, uint8_t* out, mpfa_stream_t stream) {
-  const bool fmt_ok = (fmt >= 0 && fmt <= 3) || (fmt >= 0x101 && fmt <= 0x17E) || (fmt >= 0x201 && fmt <= 0x2FE);
+  const bool fmt_ok = (fmt >= 0 && fmt <= 3) || (fmt >= 0x101 && fmt <= 0x17E) || (fmt >= 0x201 && fmt <= 0x2FE) ||
+                      (fmt >= 0x301 && fmt <= 0x37E) || (fmt >= 0x401 && fmt <= 0x4FE);
   if (!fmt_ok || n < 0 || (n > 0 && (!x || !out))) return MPFA_ERR_INVALID;
   if (n > (int64_t)UINT32_MAX * 256) return MPFA_ERR_INVALID;
   return mpfa::launch_convert(fmt, x, n, out, reinterpret_cast<hipStream_t>(stream)) == hipSuccess

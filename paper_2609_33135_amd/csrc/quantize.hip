@@ -670,7 +670,11 @@ __global__ void convert_kernel(int fmt, const float* x, int64_t n, uint8_t* out)
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   uint32_t c;
-  if (fmt >= 0x200) {   // MXFP4 element: x / 2^e, e = (fmt & 0xFF) - 127 >= -126
+  if (fmt >= 0x400) {   // reference for 0x200 + b: exact scaling, then the software encoder
+    c = e2m1_rne_sat(__builtin_ldexpf(x[i], 127 - (fmt & 0xFF)));
+  } else if (fmt >= 0x300) {   // reference for 0x100 + c: IEEE division, then the software encoder
+    c = e2m1_rne_sat(__fdiv_rn(x[i], e4m3_value(fmt & 0xFF)));
+  } else if (fmt >= 0x200) {   // MXFP4 element: x / 2^e, e = (fmt & 0xFF) - 127 >= -126
     c = fp4_pair(0u, x[i], 0.0f, __builtin_ldexpf(1.0f, (fmt & 0xFF) - 127), 0) & 0xFu;
   } else if (fmt >= 0x100) {   // NVFP4 element: x / e4m3_value(fmt & 0xFF), the quantizer's division
     const float s = e4m3_value(fmt & 0xFF), r = __fdiv_rn(1.0f, s);

@@ -190,7 +190,7 @@ def test_quantize_validation(mp):
 
 
 def test_convert_validation(mp):
-    for bad in (4, -1, 0x100, 0x17F, 0x200, 0x2FF, 0x300):
+    for bad in (4, -1, 0x100, 0x17F, 0x200, 0x2FF, 0x300, 0x37F, 0x400, 0x4FF, 0x500):
         assert mp.lib().mpfa_convert(bad, None, 0, None, None) == 1, bad
     assert mp.lib().mpfa_convert(0, None, 5, None, None) == 1
 
