@@ -554,7 +554,8 @@ __device__ __forceinline__ void store_output(const PrefillParams& p, const ItemS
 // workgroup of kThreads threads; `bid` is the item's position in the dispatch
 // order (largest tiles first) and smem two tile buffers in LDS.  Every wave
 // runs QK, softmax and PV of a tile back to back; the next tile is fetched
-// into registers meanwhile and stored to the other buffer at the end.
+// into registers meanwhile (two tiles ahead for MXFP4) and stored to the other
+// buffer at the end.
 template <int SEED, bool MX, int PV, int ABL = 0>
 __device__ __forceinline__ void prefill_item(const PrefillParams& p, int bid, PrefillSmemT<PV>* smem) {
   ItemState<> st;
@@ -575,6 +576,38 @@ __device__ __forceinline__ void prefill_item(const PrefillParams& p, int bid, Pr
     TileRegs<PV> r0r;
     fetch_tile<MX, PV>(r0r, p, pt, st.hk, st.h, st.j_hi, st.kvl, threadIdx.x);
     store_tile<MX, PV>(smem[st.j_hi & 1], r0r, st.seed_scale, threadIdx.x);
+  }
+  if constexpr (MX && SEED != kSeedElem) {
+    // MXFP4 keeps two fetched tiles in registers (its register budget allows
+    // it, except with the element-wise compensation): tile j-2 is loaded during step j and stored at the end of step j-1,
+    // so its loads have two steps to arrive.  The loop is unrolled twice so the
+    // two register sets keep fixed names.
+    TileRegs<PV> ra, rb;
+    if (st.j_hi >= 1) fetch_tile<MX, PV>(ra, p, pt, st.hk, st.h, st.j_hi - 1, st.kvl, threadIdx.x);
+    __syncthreads();
+    auto step = [&](int j, const TileRegs<PV>& held, TileRegs<PV>& fresh) {
+      if (j >= 2) fetch_tile<MX, PV>(fresh, p, pt, st.hk, st.h, j - 2, st.kvl, threadIdx.x);
+      const PrefillSmemT<PV>& sm = smem[j & 1];
+      const int key0 = j * kTile;
+      if (st.wave_active && key0 <= st.wpos_max) {
+        f32x4 s[8][kNB];
+        qk_tile<SEED, MX, PV>(s, sm, st);
+        PTile<> ptile;
+        softmax_tile<PV, ABL>(s, key0, key0 + kTile - 1 > st.wpos_min, st, m, l, o, ptile);
+        pv_tile<PV>(sm, ptile, o, st);
+      }
+      if (j >= 1) store_tile<MX, PV>(smem[(j - 1) & 1], held, st.seed_scale, threadIdx.x);
+      __syncthreads();
+    };
+    int j = st.j_hi;
+    for (; j >= 1; j -= 2) {
+      step(j, ra, rb);
+      step(j - 1, rb, ra);
+    }
+    if (j == 0) step(0, ra, rb);
+    if (!st.wave_active) return;
+    store_output(p, st, l, o);
+    return;
   }
   __syncthreads();
   for (int j = st.j_hi; j >= 0; --j) {
