@@ -35,8 +35,9 @@
  *    q_start >= 0 and q_start + query tokens <= kv_len <= 64 max_pages; decode
  *    kv_len >= 1 and within max_partitions partitions; page-table entries of
  *    the pages in use >= 0, and < num_pages when the arguments carry it.
- *  - The library holds no mutable global state; concurrent calls on
- *    different streams are safe when their output buffers do not overlap.
+ *  - The library holds no mutable global state apart from the per-GPU scratch
+ *    of mpfa_decode_paged_static; concurrent calls of the other entry points
+ *    on different streams are safe when their output buffers do not overlap.
  *
  * Layouts (head_dim D = 128, 16-element NVFP4 groups, 64-token pages):
  *  - Q, K, V inputs: bf16 [T][H][128], tokens of all sequences packed,
