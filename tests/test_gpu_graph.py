@@ -3,7 +3,9 @@ split-KV workspaces are preallocated so that decode can be captured into a
 graph and replayed).
 
 prefill, paged decode and the one-launch mixed step are captured together
-through torch.cuda.CUDAGraph on one stream, with every buffer (workspaces
+through torch.cuda.CUDAGraph on one stream (and, in a second graph, the whole
+path: quantization with statistics, prefill, the decode step's cache write and
+the decode), with every buffer (workspaces
 included) allocated and initialised before the capture; the graph is then
 replayed several times, with the program's own eager launches and host
 synchronisations between the replays, and every replay must reproduce the
@@ -94,4 +96,78 @@ def test_graph_capture_and_replay(orc, mp):
         mp.decode_paged(qd, run.cache, run.stats, kv, pt, eager_out, part, maxp, ws, mp.SMOOTH)
         torch.cuda.synchronize()
         assert np.array_equal(H.bits(eager_out), want_dec), f"eager decode after replay {rep}"
+    print("graph replays identical", flush=True)
+
+
+def test_graph_whole_path(orc, mp):
+    """The whole path in one graph: the first quantization call (statistics
+    computed, cache written), the causal prefill over that cache, then a decode
+    step: the cache write of one new token per sequence with the frozen
+    statistics (Sec. 6) and the paged decode.  Before every replay the graph's
+    cache, statistics and outputs are cleared by eager fills, so each replay
+    must rewrite them; all of them must match the eager run byte for byte."""
+    print("case: graph capture of quantize + prefill + append + decode", flush=True)
+    seqlens = [200, 65, 130]
+    h_q, h_kv, part = 8, 2, 128
+    run = H.Run(orc, mp, 103, seqlens, h_q, h_kv)
+    B = run.B
+    T = int(run.cu[-1])
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+    pos = np.asarray(seqlens)                       # the new token of each sequence
+    assert all(int(p) // 64 < (n + 63) // 64 for p, n in zip(pos, seqlens))
+    slots1 = dev(np.concatenate([H.slots_for(run.pt, b, [int(pos[b])]) for b in range(B)]))
+    cu1 = dev(np.arange(B + 1, dtype=np.int32))
+    q1, k1, v1 = H.gen_qkv(104, [1] * B, h_q, h_kv, True, "cuda")
+    kv = dev((pos + 1).astype(np.int32))
+    kv0 = dev(np.asarray(seqlens, np.int32))
+    q_start = dev(np.zeros(B, np.int32))
+    pt = dev(run.pt)
+    maxp = int(max((pos + 1 + part - 1) // part))
+    ws = torch.zeros(mp.decode_workspace_size(B, h_q, maxp) // 4, dtype=torch.float32, device="cuda")
+
+    # eager reference on the Run's buffers (its first quantization call already ran)
+    want_pre = run.prefill_gpu()
+    qd = mp.QuantQ(B, B, h_q, "cuda")
+    mp.quantize_qk(q1, k1, v1, cu1, slots1, run.cache, run.stats, qd, mp.SMOOTH, 1)
+    dec = torch.empty((B, h_q, 128), dtype=torch.bfloat16, device="cuda")
+    mp.decode_paged(qd, run.cache, run.stats, kv, pt, dec, part, maxp, ws, mp.SMOOTH)
+    torch.cuda.synchronize()
+    want_dec = H.bits(dec)
+    planes = lambda c, s, qq, qd_: [c.k_codes, c.k_scales, c.v_codes, c.ds, s.q_mean, s.k_mean, s.k_tscale,
+                                    qq.codes, qq.scales, qq.tscale, qd_.codes, qd_.scales, qd_.tscale]
+    want = [t.detach().clone() for t in planes(run.cache, run.stats, run.qq, qd)]
+
+    # graph buffers: all allocated before the capture
+    cache = mp.PagedCache(run.cache.num_pages, h_q, h_kv, "cuda", smooth=True)
+    stats = mp.SeqStats(B, h_q, h_kv, "cuda")
+    qq = mp.QuantQ(T, B, h_q, "cuda")
+    qd2 = mp.QuantQ(B, B, h_q, "cuda")
+    pre = torch.empty((T, h_q, 128), dtype=torch.bfloat16, device="cuda")
+    dec2 = torch.empty((B, h_q, 128), dtype=torch.bfloat16, device="cuda")
+    ws2 = torch.zeros_like(ws)
+    torch.cuda.synchronize()
+
+    def step():
+        mp.quantize_qk(run.q, run.k, run.v, run.cu_d, run.slots_d, cache, stats, qq, run.flags, max(seqlens))
+        mp.prefill(qq, cache, stats, run.cu_d, q_start, kv0, pt, pre, max(seqlens), mp.SMOOTH)
+        mp.quantize_qk(q1, k1, v1, cu1, slots1, cache, stats, qd2, mp.SMOOTH, 1)
+        mp.decode_paged(qd2, cache, stats, kv, pt, dec2, part, maxp, ws2, mp.SMOOTH)
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    print("graph captured", flush=True)
+    for rep in range(3):
+        for t in planes(cache, stats, qq, qd2):
+            t.zero_()
+        pre.fill_(float("nan"))
+        dec2.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(planes(cache, stats, qq, qd2), want)):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), f"replay {rep}: plane {i}"
+        assert np.array_equal(H.bits(pre), want_pre), f"replay {rep}: prefill"
+        assert np.array_equal(H.bits(dec2), want_dec), f"replay {rep}: decode"
     print("graph replays identical", flush=True)
