@@ -198,7 +198,6 @@ __device__ __forceinline__ void fin_load(const QuantParams& p, int64_t t0, int n
 
 __global__ __launch_bounds__(kFinThreads) void stats_final_kernel(QuantParams p) {
   __shared__ float4 chunk[3 * kFinChunk * (kFinSlice / 4)];   // [sum, max, min][block][channel / 4]: 96 KB
-  __shared__ float red[4];
   const int hh = blockIdx.x >> 2, slice = blockIdx.x & 3, b = blockIdx.y, t = threadIdx.x;
   const int64_t t0 = p.cu_seqlens[b];
   const int n = p.cu_seqlens[b + 1] - (int)t0;
