@@ -293,6 +293,33 @@ def run_decode(mp, st):
                     st["part"], st["maxp"], st["ws"], st["flags"])
 
 
+def decode_graph_replay(torch, mp, st, steps, warmup):
+    """The decode step (partition kernel + merge) captured once in a HIP graph
+    and replayed, as a serving loop runs it (the split-KV workspace is
+    preallocated, Sec. 5.3 / Sec. 6).  Every replay's output must equal the
+    eager launch's bytes."""
+    run_decode(mp, st)
+    torch.cuda.synchronize()
+    want = st["out"].clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run_decode(mp, st)
+    torch.cuda.synchronize()
+    for _ in range(max(warmup, 1)):
+        g.replay()
+    torch.cuda.synchronize()
+    if not torch.equal(st["out"].view(torch.int16), want.view(torch.int16)):
+        raise RuntimeError("decode graph replay differs from the eager launch")
+    ts = []
+    for _ in range(steps):
+        with Timer(torch) as t:
+            g.replay()
+        ts.append(t)
+    torch.cuda.synchronize()
+    ms = sum(t.ms() for t in ts) / steps
+    return {"ms": ms, "ms_min": min(t.ms() for t in ts), "GB/s": decode_bytes(st) / (ms * 1e-3) / 1e9}
+
+
 def decode_bytes(st):
     """Algorithmic bytes of one decode launch: K codes + scales + V codes + Delta_S of
     every key (none without smoothing), the quantized queries, the outputs, the
@@ -784,6 +811,7 @@ def main():
         decode_ms = sum(t.ms() for t in ts) / args.steps
         nbytes = decode_bytes(sd)
         gbs = nbytes / (decode_ms * 1e-3) / 1e9
+        graph = decode_graph_replay(torch, mp, sd, args.steps, args.warmup)
         if not args.no_cpu_baseline:
             cpu_dec = cpu_baseline_decode(np, W, sd)
             res.setdefault("cpu_baseline", {"kind": "oracle"})["decode"] = cpu_dec
@@ -791,7 +819,7 @@ def main():
                          "frac_hbm": gbs * 1e9 / PEAK_HBM,
                          "bytes": nbytes, "traffic": measured_traffic("decode_kernel"),
                          "partition_tokens": sd["part"],
-                         "keys": int(sum(sd["lens"]))}
+                         "keys": int(sum(sd["lens"])), "graph": graph}
         del sd
         torch.cuda.empty_cache()
         if not args.no_direct:
