@@ -159,7 +159,7 @@ void orc_bf16_encode_f32_array(const float* x, int64_t n, uint16_t* out)
 }
 
 /* -------------------------------------------------------------------------- */
-/* Quantization pass (Algorithm 1 lines before the main loop)                  */
+/* Quantization pass (the steps of Algorithm 1 before its main loop)           */
 /* -------------------------------------------------------------------------- */
 
 /* Second-level scale of NVFP4: a power of two chosen so that the largest
