@@ -230,6 +230,8 @@ __global__ __launch_bounds__(kFinThreads) void stats_final_kernel(QuantParams p)
       if (t < kFinSlice) {
         const float* cs = reinterpret_cast<const float*>(chunk);
         const int nb = min(kFinChunk, nblk - blk0);
+        // unrolled so that the LDS reads run ahead of the dependent additions
+#pragma unroll 16
         for (int j = 0; j < nb; ++j) {
           tot += cs[j * kFinSlice + t];
           mx = fmaxf(mx, cs[(kFinChunk + j) * kFinSlice + t]);
