@@ -56,12 +56,13 @@ def test_prefill_ragged_gqa(orc, mp, smooth):
     _check(run, out, _all_items(seqlens, 8), label=f"ragged smooth={smooth}")
 
 
-def test_prefill_chunked_over_prefix(orc, mp):
+@pytest.mark.parametrize("mx", [False, True])
+def test_prefill_chunked_over_prefix(orc, mp, mx):
     """Chunked prefill: the queries are the last 200 tokens of a 700-token sequence
-    (q_start = 500) attending to the whole paged prefix."""
-    print("case: chunked prefill", flush=True)
+    (q_start = 500) attending to the whole paged prefix (NVFP4 and MXFP4)."""
+    print(f"case: chunked prefill mx={mx}", flush=True)
     seqlens = [700]
-    run = H.Run(orc, mp, 23, seqlens, 4, 1, outliers=True)
+    run = H.Run(orc, mp, 23, seqlens, 4, 1, outliers=True, mxfp4=mx)
     # queries: rows 500..699 of the quantized Q, re-based as a 200-token call
     mp_ = mp
     qq = mp_.QuantQ(200, 1, 4, "cuda")
@@ -72,13 +73,14 @@ def test_prefill_chunked_over_prefix(orc, mp):
     out = torch.full((200, 4, 128), float("nan"), dtype=torch.bfloat16, device="cuda")
     mp_.prefill(qq, run.cache, run.stats, cu, torch.tensor([500], dtype=torch.int32, device="cuda"),
                 torch.tensor([700], dtype=torch.int32, device="cuda"),
-                torch.from_numpy(run.pt).cuda(), out, 200, mp_.SMOOTH)
+                torch.from_numpy(run.pt).cuda(), out, 200, mp_.SMOOTH | (mp_.MXFP4 if mx else 0))
     torch.cuda.synchronize()
     got = H.bits(out)
     r = run.ref
     items = np.array([(0, i, h) for i in range(200) for h in range(4)], np.int32)
     o16, _ = orc.prefill(r["cache"], run.pt, [700], r["k_tscale"], r["q_codes"][500:700],
-                         r["q_scales"][500:700], r["q_tscale"], [0, 200], [500], items)
+                         r["q_scales"][500:700], r["q_tscale"], [0, 200], [500], items,
+                         mxfp4=mx)
     max_abs, mean_rel, n_bad = H.compare_bf16(got.reshape(-1, 128), o16)
     print(f"chunked: max|d| {max_abs:.3e} mean rel {mean_rel:.3e}")
     assert mean_rel <= H.TOL_MEAN_REL and n_bad == 0, (n_bad, max_abs)
