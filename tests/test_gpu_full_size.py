@@ -9,7 +9,8 @@ sampled outputs one by one:
     every query head of the shortest, the longest and one middle sequence;
   * the same decode with all 32 contexts at 131072 keys (partition 4096), and
     over an MXFP4 K cache;
-  * the MXFP4 variant of the 131072-token prefill;
+  * the MXFP4 variant and the BF16 / NVFP4 PV precision assignments of the
+    131072-token prefill;
   * the mixed serving step (Qwen shapes): a 32768-token chunk at position
     65536 over its paged prefix, plus 64 decode sequences, one launch sequence
     on one stream; sampled chunk rows and sampled decode sequences.
@@ -202,6 +203,37 @@ def test_qwen_prefill_131072_mxfp4(orc, mp, bench, W):
     o16, _ = orc.prefill(rc, st["pt"], [seq], ref["k_tscale"], ref["q_codes"], ref["q_scales"],
                          ref["q_tscale"], [0, seq], [0], items, mxfp4=True)
     _report(f"qwen prefill {seq} mxfp4", out[items[:, 1], items[:, 2]], o16)
+
+
+@pytest.mark.parametrize("pv", ["bf16", "nvfp4"])
+def test_qwen_prefill_131072_pv_precisions(orc, mp, bench, W, pv):
+    """The two other PV precision assignments (Sec. 3.1) at the full Qwen size in
+    the benchmark's launch (precision_assignments): the V copy they read bit for
+    bit, sampled rows of four heads."""
+    seq = 131072
+    print(f"case: qwen prefill {seq} pv={pv} full-size (bench launch)", flush=True)
+    flag = mp.PV_BF16 if pv == "bf16" else mp.PV_NVFP4
+    st = bench.setup_prefill(torch, np, mp, W, seq, smooth=True, pv=flag)
+    bench.run_quant(mp, st)
+    bench.run_prefill(mp, st)
+    torch.cuda.synchronize()
+    out = H.bits(st["out"])
+    oflag = orc.PV_BF16 if pv == "bf16" else orc.PV_NVFP4
+    ref = orc.quantize_qk(H.bits(st["q"]), H.bits(st["k"]), H.bits(st["v"]),
+                          np.array([0, seq], np.int32), W.slots_for(st["pt"], 0, range(seq)),
+                          st["n_pages"], orc.SMOOTH | orc.COMPUTE_STATS | oflag)
+    print("oracle quantization done", flush=True)
+    rc = ref["cache"]
+    got_aux = H.bits(st["cache"].v_aux) if pv == "bf16" else st["cache"].v_aux.cpu().numpy()
+    assert np.array_equal(got_aux.reshape(-1), np.asarray(rc["v_aux"]).reshape(-1))
+    rng = np.random.default_rng(5)
+    rows = np.unique(np.concatenate([np.arange(0, 130, 11), rng.integers(0, seq, 16),
+                                     np.arange(seq - 130, seq, 17), [seq - 1]]))
+    heads = [0, 13, 27, 39]
+    items = np.array([(0, int(r), h) for r in rows for h in heads], np.int32)
+    o16, _ = orc.prefill(rc, st["pt"], [seq], ref["k_tscale"], ref["q_codes"], ref["q_scales"],
+                         ref["q_tscale"], [0, seq], [0], items, pv=oflag)
+    _report(f"qwen prefill {seq} pv {pv}", out[items[:, 1], items[:, 2]], o16)
 
 
 def test_mixed_step_qwen(orc, mp, W):
