@@ -9,8 +9,9 @@ sampled outputs one by one:
     every query head of the shortest, the longest and one middle sequence;
   * the same decode with all 32 contexts at 131072 keys (partition 4096), and
     over an MXFP4 K cache;
-  * the MXFP4 variant and the BF16 / NVFP4 PV precision assignments of the
-    131072-token prefill;
+  * the MXFP4 variant, the BF16 / NVFP4 PV precision assignments, the other
+    compensation placements and the unsmoothed variant of the 131072-token
+    prefill;
   * the mixed serving step (Qwen shapes): a 32768-token chunk at position
     65536 over its paged prefix, plus 64 decode sequences, one launch sequence
     on one stream; sampled chunk rows and sampled decode sequences.
@@ -203,6 +204,53 @@ def test_qwen_prefill_131072_mxfp4(orc, mp, bench, W):
     o16, _ = orc.prefill(rc, st["pt"], [seq], ref["k_tscale"], ref["q_codes"], ref["q_scales"],
                          ref["q_tscale"], [0, seq], [0], items, mxfp4=True)
     _report(f"qwen prefill {seq} mxfp4", out[items[:, 1], items[:, 2]], o16)
+
+
+def test_qwen_prefill_131072_placements_and_direct(orc, mp, bench, W):
+    """The other launches the benchmark times at the full Qwen size: the rank-one
+    BF16 MFMA seed gives the default kernel's bytes; the element-wise placement
+    (scores rounded in another FP32 order, so a P code near an FP8 rounding
+    boundary may fall the other way) matches the oracle on sampled rows; the
+    direct (unsmoothed) variant matches the oracle without compensation on
+    sampled rows."""
+    seq = 131072
+    print(f"case: qwen prefill {seq} placements + direct (bench launches)", flush=True)
+    st = bench.setup_prefill(torch, np, mp, W, seq, smooth=True)
+    bench.run_quant(mp, st)
+    bench.run_prefill(mp, st)
+    torch.cuda.synchronize()
+    base = H.bits(st["out"]).copy()
+    st["flags"] = mp.SMOOTH | mp.SEED_MFMA
+    bench.run_prefill(mp, st)
+    torch.cuda.synchronize()
+    assert np.array_equal(H.bits(st["out"]), base), "rank-one MFMA seed"
+    st["flags"] = mp.SMOOTH | mp.SEED_ELEMWISE
+    bench.run_prefill(mp, st)
+    torch.cuda.synchronize()
+    ew = H.bits(st["out"]).copy()
+    rng = np.random.default_rng(6)
+    rows = np.unique(np.concatenate([np.arange(0, 130, 13), rng.integers(0, seq, 12),
+                                     np.arange(seq - 130, seq, 19), [seq - 1]]))
+    heads = [3, 17, 38]
+    items = np.array([(0, int(r), h) for r in rows for h in heads], np.int32)
+    ref = orc.quantize_qk(H.bits(st["q"]), H.bits(st["k"]), H.bits(st["v"]),
+                          np.array([0, seq], np.int32), W.slots_for(st["pt"], 0, range(seq)),
+                          st["n_pages"], orc.SMOOTH | orc.COMPUTE_STATS)
+    o16, _ = orc.prefill(ref["cache"], st["pt"], [seq], ref["k_tscale"], ref["q_codes"], ref["q_scales"],
+                         ref["q_tscale"], [0, seq], [0], items)
+    _report(f"qwen prefill {seq} element-wise", ew[items[:, 1], items[:, 2]], o16)
+    del ref
+    # direct: quantization and attention without the smoothing
+    sd = bench.setup_prefill(torch, np, mp, W, seq, smooth=False)
+    bench.run_quant(mp, sd)
+    bench.run_prefill(mp, sd)
+    torch.cuda.synchronize()
+    ref = orc.quantize_qk(H.bits(sd["q"]), H.bits(sd["k"]), H.bits(sd["v"]),
+                          np.array([0, seq], np.int32), W.slots_for(sd["pt"], 0, range(seq)),
+                          sd["n_pages"], orc.COMPUTE_STATS)
+    o16, _ = orc.prefill(ref["cache"], sd["pt"], [seq], ref["k_tscale"], ref["q_codes"], ref["q_scales"],
+                         ref["q_tscale"], [0, seq], [0], items, smooth=False)
+    _report(f"qwen prefill {seq} direct", H.bits(sd["out"])[items[:, 1], items[:, 2]], o16)
 
 
 @pytest.mark.parametrize("pv", ["bf16", "nvfp4"])
