@@ -7,8 +7,8 @@ sampled outputs one by one:
     quantizer output compared bit for bit, sampled rows of several heads;
   * Llama-3.1-8B-shaped paged decode, batch 32, contexts U[16384, 131072]:
     every query head of the shortest, the longest and one middle sequence;
-  * the same decode with all 32 contexts at 131072 keys (partition 4096), and
-    over an MXFP4 K cache;
+  * the same decode with all 32 contexts at 131072 keys (partition 4096), over
+    an MXFP4 K cache, and over an unsmoothed cache;
   * the MXFP4 variant, the BF16 / NVFP4 PV precision assignments, the other
     compensation placements and the unsmoothed variant of the 131072-token
     prefill;
@@ -60,7 +60,7 @@ def _report(label, got, ref):
     assert mean_rel <= H.TOL_MEAN_REL and n_bad == 0, (label, n_bad, max_abs, mean_rel)
 
 
-def _oracle_sequence_cache(orc, W, seed, b, ctx, h_q, h_kv, outliers, device="cuda", mx=False):
+def _oracle_sequence_cache(orc, W, seed, b, ctx, h_q, h_kv, outliers, device="cuda", mx=False, smooth=True):
     """Oracle cache of one sequence's context (its own contiguous pages; the result
     does not depend on the physical page order), statistics computed on it."""
     q, k, v = W.gen_qkv(seed, [ctx], h_q, h_kv, outliers, device, seq_ids=[b])
@@ -68,23 +68,24 @@ def _oracle_sequence_cache(orc, W, seed, b, ctx, h_q, h_kv, outliers, device="cu
     pt = np.arange(npg, dtype=np.int32).reshape(1, npg)
     slots = np.arange(ctx, dtype=np.int64)
     ref = orc.quantize_qk(H.bits(q), H.bits(k), H.bits(v), np.array([0, ctx], np.int32), slots, npg,
-                          orc.SMOOTH | orc.COMPUTE_STATS | (orc.MXFP4 if mx else 0))
+                          (orc.SMOOTH if smooth else 0) | orc.COMPUTE_STATS | (orc.MXFP4 if mx else 0))
     del q, k, v
     return ref, pt
 
 
-def _oracle_decode_one(orc, W, seed, b, kv, h_q, h_kv, outliers, partition, mx=False):
+def _oracle_decode_one(orc, W, seed, b, kv, h_q, h_kv, outliers, partition, mx=False, smooth=True):
     ctx = kv - 1
-    ref0, pt = _oracle_sequence_cache(orc, W, seed, b, ctx, h_q, h_kv, outliers, mx=mx)
+    ref0, pt = _oracle_sequence_cache(orc, W, seed, b, ctx, h_q, h_kv, outliers, mx=mx, smooth=smooth)
     qn, kn, vn = W.gen_qkv(seed, [1], h_q, h_kv, outliers, "cuda", tok_offsets=[ctx], seq_ids=[b])
     ref = orc.quantize_qk(H.bits(qn), H.bits(kn), H.bits(vn), np.array([0, 1], np.int32),
-                          np.array([ctx], np.int64), pt.shape[1], orc.SMOOTH | (orc.MXFP4 if mx else 0),
+                          np.array([ctx], np.int64), pt.shape[1],
+                          (orc.SMOOTH if smooth else 0) | (orc.MXFP4 if mx else 0),
                           q_mean=ref0["q_mean"], k_mean=ref0["k_mean"], k_tscale=ref0["k_tscale"],
                           cache=ref0["cache"])
     items = np.array([(0, h) for h in range(h_q)], np.int32)
     o16, _ = orc.decode(ref["cache"], pt, np.array([kv], np.int32), ref["k_tscale"],
                         ref["q_codes"], ref["q_scales"], ref["q_tscale"], partition, items,
-                        smooth=True, mxfp4=mx)
+                        smooth=smooth, mxfp4=mx)
     return o16
 
 
@@ -159,11 +160,12 @@ def test_llama_decode_128k_partition4096(orc, mp, bench, W):
         _report(f"llama decode 128k seq {b} partition {sd['part']}", out[b], o16)
 
 
-def test_llama_decode_batch32_mxfp4(orc, mp, bench, W):
-    """The decode_mxfp4 point of the benchmark (the batch-32 Llama decode over an
-    MXFP4 K cache): the shortest, a middle and the longest sequence."""
-    print("case: llama decode batch 32 mxfp4 full-size (bench launch)", flush=True)
-    sd = bench.setup_decode(torch, np, mp, W, 32, mx=True)
+@pytest.mark.parametrize("mx,smooth", [(True, True), (False, False)])
+def test_llama_decode_batch32_variants(orc, mp, bench, W, mx, smooth):
+    """The decode_mxfp4 and direct (unsmoothed cache) points of the benchmark, on
+    the batch-32 Llama decode: the shortest, a middle and the longest sequence."""
+    print(f"case: llama decode batch 32 mx={mx} smooth={smooth} full-size (bench launch)", flush=True)
+    sd = bench.setup_decode(torch, np, mp, W, 32, mx=mx, smooth=smooth)
     bench.run_decode(mp, sd)
     torch.cuda.synchronize()
     out = H.bits(sd["out"])
@@ -172,8 +174,8 @@ def test_llama_decode_batch32_mxfp4(orc, mp, bench, W):
     order = np.argsort(lens)
     for b in (int(order[0]), int(order[len(order) // 2]), int(order[-1])):
         o16 = _oracle_decode_one(orc, W, wl.seed, b, int(lens[b]), wl.h_q, wl.h_kv, wl.outliers,
-                                 sd["part"], mx=True)
-        _report(f"llama decode mxfp4 seq {b} kv {lens[b]} partition {sd['part']}", out[b], o16)
+                                 sd["part"], mx=mx, smooth=smooth)
+        _report(f"llama decode mx={mx} smooth={smooth} seq {b} kv {lens[b]}", out[b], o16)
 
 
 def test_qwen_prefill_131072_mxfp4(orc, mp, bench, W):
