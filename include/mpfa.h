@@ -347,7 +347,9 @@ mpfa_status mpfa_mixed_step(const mpfa_prefill_args* prefill, const mpfa_decode_
  * written out from their definitions (IEEE division __fdiv_rn, exact
  * power-of-two scaling ldexpf, then the fmt 1 encoder), the references the
  * quantizer's element paths are checked against.  x and out are device
- * pointers of n elements; MPFA_ERR_INVALID for another fmt. */
+ * pointers of n elements; x must be finite (the codes of NaN inputs are
+ * unspecified, as everywhere in the library); MPFA_ERR_INVALID for another
+ * fmt. */
 mpfa_status mpfa_convert(int32_t fmt, const float* x, int64_t n, uint8_t* out,
                          mpfa_stream_t stream);
 

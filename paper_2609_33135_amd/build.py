@@ -39,6 +39,9 @@ COMMON = [
 # v_max_f32 per operand, which takes about 70 VALU instructions out of every
 # 128-key tile of the prefill loop.
 EXTRA = {"prefill.hip": ["-fno-honor-nans"], "mixed.hip": ["-fno-honor-nans"],
+         # the same for the quantization pass: its max / min reductions need no
+         # quieting instruction per loaded value
+         "quantize.hip": ["-fno-honor-nans"],
          # the MFMA probe keeps its accumulators in VGPRs: with the AGPR form the
          # compiler copies them between the two register files inside the loop
          "probe.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
